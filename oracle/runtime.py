@@ -1,0 +1,128 @@
+"""Causal cache controller and the cached / uncached samplers (Sec. 3, Eq. 1, Eq. 12).
+
+Test infrastructure only (see oracle/__init__.py).
+
+Per scene and step k (Sec. 3.2):
+  * step 1 is always a full evaluation (Eq. 1 discussion);
+  * a planned full step evaluates the backbone, refreshes the cache r = h_out - h_in
+    and the reference input u_j, and resets the age;
+  * before a planned reuse (the h-th of a run started at j) the observed drift
+    d_obs = dist(u_{j+h}, u_j) / (norm(u_{j+h}) + eps) is measured before any
+    backbone call; reuse is accepted iff d_obs <= dbar_{j,h} + eps and
+    C + c_{j,h} <= tau, and then C grows by c_{j,h};
+  * otherwise the step evaluates the backbone and refreshes (C unchanged), and
+    the unexecuted suffix is replanned from age zero with budget tau - C; the
+    executed prefix is never changed.
+Reading (Eq. 12 vs the workload's stated metric): the distance is selectable:
+"l1" uses sums of absolute values, "l2" the Euclidean norms of Eq. 12; both use
+the whole per-scene video-row tensor.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from . import dit
+from .dp import schedule
+
+
+class StepRecord:
+    __slots__ = ("k", "planned", "realized", "drift", "drift_l2", "threshold", "vetoed", "j", "age")
+
+    def __init__(self, **kw):
+        for s in self.__slots__:
+            setattr(self, s, kw.get(s))
+
+
+class SampleResult:
+    def __init__(self, x, records, plans, charge):
+        self.x = x                  # final latent x_{K+1}
+        self.records = records      # StepRecord per step
+        self.plans = plans          # every schedule used (initial + replans)
+        self.charge = charge        # final accumulated charge C (2^-40 units)
+
+    @property
+    def realized(self):
+        return [r.realized for r in self.records]
+
+    def margins(self):
+        """|d_obs - threshold| at every drift check."""
+        return [abs(r.drift - r.threshold) for r in self.records if r.drift is not None]
+
+
+def drift_sums(u, u_ref):
+    """(sum|u-u_ref|, sum|u|, sum (u-u_ref)^2, sum u^2) over the whole tensor."""
+    dlt = u - u_ref
+    return (float(np.abs(dlt).sum()), float(np.abs(u).sum()),
+            float((dlt * dlt).sum()), float((u * u).sum()))
+
+
+def drift_value(sums, eps, metric="l1"):
+    s1, s2, s3, s4 = sums
+    if metric == "l1":
+        return s1 / (s2 + eps)
+    return math.sqrt(s3) / (math.sqrt(s4) + eps)
+
+
+def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=()):
+    """One cached K-step sample of one scene.
+
+    W: `Weights`; x1 [C,T,H,W]; txt [n_txt, d]; sigmas [K+1]; prob: `SchedProblem`.
+    uncached=True runs every step in full with no drift checks (the plain sampler).
+    force_veto: steps whose planned reuse is rejected regardless of the drift
+    (exercises the veto path)."""
+    P = dit.Params(W)
+    m = W.m
+    K = prob.K
+    x = x1.astype(np.float64)
+    plan = schedule(prob)
+    plans = [plan]
+    tables = plan.tables
+    mask = list(plan.reuse)
+    C = 0
+    n_done = 0
+    j = 1
+    age = 0
+    r = None
+    u_ref = None
+    records = []
+    for k in range(1, K + 1):
+        mods, head_mod = dit.step_modulation(P, sigmas[k - 1])
+        h_in = dit.embed(P, x, txt)
+        u = dit.backbone_input(P, h_in, mods[0])
+        planned = 0 if (uncached or k == 1) else mask[k - 1]
+        rec = StepRecord(k=k, planned=planned, drift=None, drift_l2=None, threshold=None,
+                         vetoed=False)
+        reuse = False
+        if planned:
+            sums = drift_sums(u, u_ref)
+            d_obs = drift_value(sums, prob.eps, metric)
+            thr = tables.threshold(j, age + 1)
+            c = tables.cost(j, age + 1)
+            rec.drift, rec.drift_l2, rec.threshold = d_obs, drift_value(sums, prob.eps, "l2"), thr
+            if k not in force_veto and d_obs <= thr + prob.eps and C + c <= prob.tau_q:
+                reuse = True
+                C += c
+                age += 1
+                n_done += 1
+            else:
+                rec.vetoed = True
+        if reuse:
+            g = h_in[: m.n_v] + r
+        else:
+            h_out = dit.backbone(P, mods, h_in)
+            r = h_out[: m.n_v] - h_in[: m.n_v]
+            g = h_out[: m.n_v]
+            u_ref = u
+            j, age = k, 0
+            if rec.vetoed:
+                newp = schedule(prob.replace(start_step=k, spent_q=C, spent_n=n_done))
+                plans.append(newp)
+                mask = mask[:k] + list(newp.reuse[k:])
+        rec.realized = 1 if reuse else 0
+        rec.j, rec.age = j, age
+        records.append(rec)
+        v = dit.head(P, head_mod, g)
+        x = dit.euler(x, v, sigmas[k - 1], sigmas[k])
+    return SampleResult(x, records, plans, C)
