@@ -1,0 +1,181 @@
+"""Benchmark: cached K-step sampling of the 30-block video DiT on one MI355X.
+
+One benchmark step = one whole cached sample of the workload: the host schedule
+(dc_sampler_create: modulation table + exact DP), then K calls of
+dc_denoise_step (patch embedding, drift checks with their readbacks, refresh
+blocks or cache reuse, head + Euler).  Inputs (weights, initial latent, text)
+are resident in HBM before the timed region.
+
+Prints one JSON line: latent tokens x steps / s = B * N_v * K / (seconds per
+sample), the roofline of the dominant kernel (attention, timed live with
+hipEvents over the timed region) and the CPU oracle's rate on a bounded sample.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MI355X_BF16_DENSE_TFLOPS = 2500.0     # published dense bf16 MFMA peak
+MI355X_HBM_GBPS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def attention_flops(m):
+    """Algorithmic FLOPs of one attention launch (one scene, all heads): QK^T and PV."""
+    return 4.0 * m.n_tok * m.n_tok * m.hidden
+
+
+def refresh_flops(m):
+    """Algorithmic FLOPs of one refresh step of one scene (blocks + patch embed + head)."""
+    N, d, F = m.n_tok, m.hidden, m.mlp_hidden
+    per_block = 2.0 * N * d * (3 * d + d + 2 * F) + attention_flops(m)
+    return m.n_blocks * per_block + 2.0 * 2 * m.n_v * 64 * d
+
+
+def cpu_baseline(w, W, schedule, budget_s=30.0):
+    """The fp64 oracle on a bounded sample of the same workload, extrapolated to one
+    cached sample: one block at full length on two query-row subsets (the per-block
+    cost is fixed key/value work plus a per-row cost) and one full reuse step."""
+    import numpy as np
+    from oracle import dit
+    from paper_2608_16354_amd import inputs as I
+
+    m = w.model
+    P = dit.Params(W)
+    mods, head_mod = dit.step_modulation(P, 0.5)
+    h = I.hidden_state(m, (90,)).astype(np.float64)
+    rng = np.random.default_rng(0)
+    times = {}
+    for R in (128, 512):
+        rows = np.sort(rng.choice(m.n_tok, R, replace=False))
+        t0 = time.perf_counter()
+        dit.block(P, 0, mods[0], h, rows=rows)
+        times[R] = time.perf_counter() - t0
+    per_row = (times[512] - times[128]) / (512 - 128)
+    fixed = max(times[128] - 128 * per_row, 0.0)
+    t_block = fixed + m.n_tok * per_row
+    x = I.latent(m, w.cfg_id, 0).astype(np.float64)
+    txt = I.text(m, w.cfg_id, 0)
+    t0 = time.perf_counter()
+    h_in = dit.embed(P, x, txt)
+    u = dit.backbone_input(P, h_in, mods[0])
+    _ = np.abs(u - u).sum()
+    g = h_in[: m.n_v] + h_in[: m.n_v]
+    dit.euler(x, dit.head(P, head_mod, g), 0.5, 0.48)
+    t_reuse = time.perf_counter() - t0
+    n_ref = sum(1 for r in schedule if not r)
+    n_reu = len(schedule) - n_ref
+    t_sample = n_ref * (m.n_blocks * t_block + t_reuse) + n_reu * t_reuse
+    cores = len(os.sched_getaffinity(0))
+    spent = sum(times.values()) + t_reuse
+    return {"value": w.batch * m.n_v * w.K / (w.batch * t_sample), "unit": "latent token*steps/s",
+            "cores": cores, "kind": "oracle",
+            "sample": (f"fp64 oracle: one block at {m.n_tok} tokens on 128 and 512 query rows "
+                       f"({times[128]:.1f}s, {times[512]:.1f}s) + one full reuse step ({t_reuse:.1f}s), "
+                       f"extrapolated to the {n_ref}-refresh/{n_reu}-reuse schedule; {spent:.0f}s of CPU work")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3, help="timed cached samples")
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="dit-30x1920-bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip the live kernel timing")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the step would shard)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_16354_amd import api
+    from paper_2608_16354_amd import inputs as I
+
+    w = I.WORKLOADS[args.workload]
+    m = w.model
+    dev = "cuda:0"
+    t0 = time.time()
+    W = I.Weights(m, w.cfg_id)
+    dm = api.DeviceModel(W, dev)
+    log(f"weights drawn and uploaded in {time.time() - t0:.1f}s")
+    cal = [I.scene_problem(w, mo) for mo in I.calibration_motions(32)]
+    tau = I.TAU_INF if w.tau == "inf" else api.dc_select_tau(cal, w.rho)
+    motions = I.scene_motions(w)
+    probs = [I.scene_problem(w, mo, tau_q=tau) for mo in motions]
+    x1 = torch.from_numpy(np.stack([I.latent(m, w.cfg_id, s) for s in range(w.batch)])).to(dev)
+    txt = torch.from_numpy(np.stack([I.text(m, w.cfg_id, s) for s in range(w.batch)])).to(dev)
+    bufs = api.SamplerBuffers(m, w.batch, w.K, dev)
+    sig = I.sigmas(w.K)
+    torch.cuda.synchronize()
+
+    def one_sample():
+        smp = api.Sampler(dm, probs, sig, x1, txt, bufs=bufs)
+        rs = []
+        for _ in range(w.K):
+            r, _ = smp.step()
+            rs.append(r)
+        smp.close()
+        return np.stack(rs)
+
+    for i in range(args.warmup):
+        one_sample()
+        torch.cuda.synchronize()
+        log(f"warmup {i + 1}/{args.warmup} done")
+    prof = api.profile(["attention"]) if not args.no_profile else None
+    torch.cuda.synchronize()
+    if prof:
+        prof.__enter__()
+    t0 = time.perf_counter()
+    masks = []
+    for i in range(args.steps):
+        masks.append(one_sample())
+        log(f"timed sample {i + 1}/{args.steps}")
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    if prof:
+        prof.__exit__(None, None, None)
+        kstats = prof.read()
+    ms_per = 1000.0 * el / args.steps
+    value = w.batch * m.n_v * w.K / (ms_per / 1000.0)
+    realized = masks[-1]
+    n_refresh = int((realized == 0).sum())
+    out = {
+        "metric": "latent tokens x steps / s, cached 50-step sample",
+        "value": value, "unit": "latent token*steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": m.dtype, "data": "synthetic (seeded latents, random-init weights)",
+        "config": {"workload": w.name, "blocks": m.n_blocks, "hidden": m.hidden, "heads": m.heads,
+                   "video_tokens": m.n_v, "text_tokens": m.n_txt, "denoise_steps": w.K,
+                   "batch": w.batch, "refresh_steps": n_refresh, "reuse_steps": int(realized.sum()),
+                   "tau_q": int(tau) if tau != I.TAU_INF else None},
+    }
+    if prof:
+        n, tot = kstats["attention"]
+        avg_ms = tot / max(n, 1)
+        achieved = attention_flops(m) / (avg_ms / 1000.0) / 1e12
+        out["roofline"] = {"kernel": "attention", "bound": "mfma", "achieved": achieved,
+                           "peak": MI355X_BF16_DENSE_TFLOPS, "unit": "TFLOP/s",
+                           "frac": achieved / MI355X_BF16_DENSE_TFLOPS, "traffic": None,
+                           "launches": n, "avg_ms": avg_ms}
+    # refresh FLOPs of the executed schedule over the whole sample time (reuse steps included)
+    out["sample_tflops"] = refresh_flops(m) * n_refresh / (ms_per / 1000.0) / 1e12
+    if not args.no_cpu_baseline:
+        log("cpu baseline (fp64 oracle, bounded sample)")
+        out["cpu_baseline"] = cpu_baseline(w, W, realized[:, 0].tolist())
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -36,8 +36,9 @@ class StepRecord:
 
 
 class SampleResult:
-    def __init__(self, x, records, plans, charge):
+    def __init__(self, x, records, plans, charge, plan):
         self.x = x                  # final latent x_{K+1}
+        self.plan = plan            # the plan as it stood at the end (prefix executed, suffixes replanned)
         self.records = records      # StepRecord per step
         self.plans = plans          # every schedule used (initial + replans)
         self.charge = charge        # final accumulated charge C (2^-40 units)
@@ -125,4 +126,4 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=())
         records.append(rec)
         v = dit.head(P, head_mod, g)
         x = dit.euler(x, v, sigmas[k - 1], sigmas[k])
-    return SampleResult(x, records, plans, C)
+    return SampleResult(x, records, plans, C, mask)

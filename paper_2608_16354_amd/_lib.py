@@ -1,0 +1,120 @@
+"""ctypes declarations of the C ABI in include/dc.h (argument marshalling only)."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdrivecache.so")
+
+DC_OK, DC_ERR_ARG, DC_ERR_SHAPE, DC_ERR_DTYPE, DC_ERR_HIP, DC_ERR_WORKSPACE, DC_ERR_STATE = 0, -1, -2, -3, -4, -5, -6
+DC_F32, DC_BF16 = 0, 1
+DC_MAX_BATCH = 64
+
+vp = C.c_void_p
+
+
+class ModelCfg(C.Structure):
+    _fields_ = [("n_blocks", C.c_int32), ("hidden", C.c_int32), ("heads", C.c_int32),
+                ("head_dim", C.c_int32), ("mlp_hidden", C.c_int32), ("lat_c", C.c_int32),
+                ("lat_t", C.c_int32), ("lat_h", C.c_int32), ("lat_w", C.c_int32),
+                ("patch", C.c_int32), ("n_txt", C.c_int32), ("dtype", C.c_int32),
+                ("ln_eps", C.c_float)]
+
+
+class BlockWeights(C.Structure):
+    _fields_ = [("w_qkv", vp), ("b_qkv", vp), ("w_o", vp), ("b_o", vp), ("w_1", vp), ("b_1", vp),
+                ("w_2", vp), ("b_2", vp), ("mod_offset", vp)]
+
+
+class ModelWeights(C.Structure):
+    _fields_ = [("w_pe", vp), ("b_pe", vp), ("pos", vp), ("w_t1", vp), ("b_t1", vp), ("w_t2", vp),
+                ("b_t2", vp), ("w_m", vp), ("b_m", vp), ("head_mod", vp), ("w_head", vp),
+                ("b_head", vp), ("blocks", C.POINTER(BlockWeights))]
+
+
+class SchedProblem(C.Structure):
+    _fields_ = [("K", C.c_int32), ("h_max", C.c_int32), ("n_cap", C.c_int32),
+                ("legal", C.POINTER(C.c_uint8)), ("segment", C.POINTER(C.c_int32)),
+                ("n_pose", C.c_int32), ("pose_xy", C.POINTER(C.c_double)),
+                ("pose_yaw", C.POINTER(C.c_double)), ("L0", C.c_double), ("Th0", C.c_double),
+                ("L1", C.c_double), ("Th1", C.c_double), ("eps", C.c_double),
+                ("q0", C.POINTER(C.c_double)), ("q1", C.POINTER(C.c_double)),
+                ("d0", C.POINTER(C.c_double)), ("d1", C.POINTER(C.c_double)),
+                ("tau_q", C.c_int64), ("start_step", C.c_int32), ("spent_q", C.c_int64),
+                ("spent_n", C.c_int32)]
+
+
+class Schedule(C.Structure):
+    _fields_ = [("reuse", C.POINTER(C.c_uint8)), ("chat_q", C.POINTER(C.c_int64)),
+                ("dbar", C.POINTER(C.c_double)), ("n_reuse", C.c_int32), ("cost_q", C.c_int64),
+                ("L", C.c_double), ("Theta", C.c_double), ("zL", C.c_double), ("zTh", C.c_double),
+                ("D", C.c_double), ("in_support", C.c_int32)]
+
+
+class Buffers(C.Structure):
+    _fields_ = [("x", vp), ("txt", vp), ("h_in", vp), ("h", vp), ("resid", vp), ("u_ref", vp),
+                ("mod", vp), ("sums", vp), ("ws", vp), ("ws_bytes", C.c_size_t)]
+
+
+P = C.POINTER
+i32p = P(C.c_int32)
+
+SIGNATURES = {
+    "dc_last_error": (C.c_char_p, []),
+    "dc_workspace_bytes": (C.c_size_t, [P(ModelCfg), C.c_int32]),
+    "dc_time_modulation": (C.c_int32, [P(ModelCfg), P(ModelWeights), P(C.c_double), C.c_int32, vp, vp,
+                                       C.c_size_t, vp]),
+    "dc_patch_embed": (C.c_int32, [P(ModelCfg), P(ModelWeights), vp, vp, vp, i32p, C.c_int32, vp,
+                                   C.c_size_t, vp]),
+    "dc_block_forward": (C.c_int32, [P(ModelCfg), P(BlockWeights), vp, vp, i32p, C.c_int32, vp,
+                                     C.c_size_t, vp]),
+    "dc_cache_store": (C.c_int32, [P(ModelCfg), vp, vp, vp, i32p, C.c_int32, vp]),
+    "dc_cache_apply": (C.c_int32, [P(ModelCfg), vp, vp, vp, i32p, C.c_int32, vp]),
+    "dc_drift_l1": (C.c_int32, [P(ModelCfg), vp, vp, vp, C.c_int32, vp, i32p, C.c_int32, vp,
+                                C.c_size_t, vp]),
+    "dc_head_euler": (C.c_int32, [P(ModelCfg), P(ModelWeights), vp, vp, vp, C.c_float, i32p,
+                                  C.c_int32, vp, C.c_size_t, vp]),
+    "dc_schedule_dp": (C.c_int32, [P(SchedProblem), P(Schedule)]),
+    "dc_select_tau": (C.c_int32, [P(SchedProblem), C.c_int32, C.c_double, P(C.c_int64)]),
+    "dc_sampler_create": (C.c_int32, [P(ModelCfg), P(ModelWeights), C.c_int32, P(SchedProblem),
+                                      P(C.c_double), P(Buffers), C.c_int32, vp, P(vp)]),
+    "dc_denoise_step": (C.c_int32, [vp, C.c_int32, vp, P(C.c_uint8), P(C.c_double)]),
+    "dc_sampler_plan": (C.c_int32, [vp, C.c_int32, P(C.c_uint8), i32p, P(C.c_int64)]),
+    "dc_sampler_destroy": (None, [vp]),
+    "dc_profile_enable": (C.c_int32, [C.c_uint32]),
+    "dc_profile_read": (C.c_int32, [C.c_int32, P(C.c_int64), P(C.c_double)]),
+    "dc_profile_reset": (C.c_int32, []),
+}
+
+KERNEL_CLASSES = ("attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "ln_modulate",
+                  "patch_embed", "drift", "cache_store", "cache_apply", "head")
+
+_lib = None
+
+
+class DriveCacheError(RuntimeError):
+    def __init__(self, fn, code, msg):
+        super().__init__(f"{fn} failed with status {code}: {msg}")
+        self.code = code
+
+
+def load() -> C.CDLL:
+    """Load libdrivecache.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with python -m paper_2608_16354_amd.build")
+        lib = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(lib, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def check(fn: str, code: int):
+    if code != DC_OK:
+        msg = load().dc_last_error().decode(errors="replace")
+        raise DriveCacheError(fn, code, msg)

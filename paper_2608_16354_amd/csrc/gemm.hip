@@ -1,0 +1,330 @@
+// GEMMs of the denoising step: C = A W^T with fused epilogues.
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16 tiles (gfx950), 256 threads = 4 waves,
+// block tile BM x BN x 64, double-buffered LDS with an XOR swizzle on the 16-byte
+// chunks of each 128-byte row (so the 8 rows read by 8 consecutive lanes hit 8
+// different chunks), one barrier per k-step, the next k-tile prefetched into
+// registers while the current one is multiplied.
+// f32 path: a plain SIMT tiled kernel for the fp32 model and the small
+// fp32 GEMMs (patch embedding, timestep MLP).
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace dc {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ inline uint16_t to_bf16(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+__device__ inline float from_bf16(uint16_t u) { return __uint_as_float(uint32_t(u) << 16); }
+
+// GELU with the tanh approximation, written as z * sigmoid(2y), y = sqrt(2/pi)(z + 0.044715 z^3)
+// (0.5 (1 + tanh y) = 1 / (1 + exp(-2y))).
+__device__ inline float gelu_tanh(float z) {
+  const float y = 0.7978845608028654f * (z + 0.044715f * z * z * z);
+  return z / (1.0f + __expf(-2.0f * y));
+}
+__device__ inline float silu(float z) { return z / (1.0f + expf(-z)); }
+
+// ---------------------------------------------------------------------------
+// epilogues: operator()(m, n, acc) for one output element
+// ---------------------------------------------------------------------------
+struct EpiQKVBf16 {
+  const float* bias; uint16_t* qk; uint16_t* vt; int d; int ldv;
+  __device__ void operator()(int m, int n, float v) const {
+    v += bias[n];
+    if (n < 2 * d) qk[size_t(m) * 2 * d + n] = to_bf16(v);
+    else vt[size_t(n - 2 * d) * ldv + m] = to_bf16(v);
+  }
+};
+struct EpiQKVF32 {
+  const float* bias; float* qk; float* vt; int d; int ldv;
+  __device__ void operator()(int m, int n, float v) const {
+    v += bias[n];
+    if (n < 2 * d) qk[size_t(m) * 2 * d + n] = v;
+    else vt[size_t(n - 2 * d) * ldv + m] = v;
+  }
+};
+struct EpiGateResidual {
+  const float* bias; const float* gate; float* h; int ldh;
+  __device__ void operator()(int m, int n, float v) const {
+    float* p = h + size_t(m) * ldh + n;
+    *p = *p + gate[n] * (v + bias[n]);
+  }
+};
+struct EpiGeluBf16 {
+  const float* bias; uint16_t* out; int ldo;
+  __device__ void operator()(int m, int n, float v) const {
+    out[size_t(m) * ldo + n] = to_bf16(gelu_tanh(v + bias[n]));
+  }
+};
+struct EpiGeluF32 {
+  const float* bias; float* out; int ldo;
+  __device__ void operator()(int m, int n, float v) const {
+    out[size_t(m) * ldo + n] = gelu_tanh(v + bias[n]);
+  }
+};
+struct EpiBiasAct {
+  const float* bias; float* out; int ldo; int act;
+  __device__ void operator()(int m, int n, float v) const {
+    v += bias[n];
+    out[size_t(m) * ldo + n] = act ? silu(v) : v;
+  }
+};
+struct EpiPatch {
+  const float* bias; const float* pos_f; const uint16_t* pos_b; float* out; int ldo;
+  __device__ void operator()(int m, int n, float v) const {
+    const size_t e = size_t(m) * ldo + n;
+    const float p = pos_b ? from_bf16(pos_b[e]) : pos_f[e];
+    out[e] = (v + bias[n]) + p;
+  }
+};
+// Head + Euler: token m, patch-vector index n -> latent element; x += dsigma * (acc + b).
+struct EpiHeadEuler {
+  const float* bias; float* x; float dsigma; int T, Hl, Wl, p, Hp, Wp;
+  __device__ void operator()(int m, int n, float v) const {
+    const int pp = p * p;
+    const int c = n / pp, a = (n / p) % p, b = n % p;
+    const int t = m / (Hp * Wp), i = (m / Wp) % Hp, j = m % Wp;
+    float* dst = x + ((size_t(c) * T + t) * Hl + (p * i + a)) * Wl + (p * j + b);
+    *dst = *dst + dsigma * (v + bias[n]);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int WN, class Epi>
+__global__ void __launch_bounds__(256) k_gemm_bf16(const uint16_t* __restrict__ A, int lda,
+                                                   const uint16_t* __restrict__ W, int ldw, int M,
+                                                   int N, int K, Epi epi) {
+  constexpr int BK = 64;
+  constexpr int WTM = BM / WM, WTN = BN / WN;     // wave tile
+  constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA tiles per wave
+  constexpr int AC = BM * 8 / 256, BC = BN * 8 / 256;   // 16-B chunks per thread
+  static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && AC >= 1 && BC >= 1, "tile shape");
+  __shared__ uint4 sA[2][BM * 8];
+  __shared__ uint4 sB[2][BN * 8];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int lc = tid & 7, lr = tid >> 3;          // loader: chunk, base row
+
+  uint4 ra[AC], rb[BC];
+  auto gload = [&](int kt) {
+    const int k0 = kt * BK + lc * 8;
+#pragma unroll
+    for (int i = 0; i < AC; ++i) {
+      const int gm = m0 + lr + 32 * i;
+      ra[i] = gm < M ? *reinterpret_cast<const uint4*>(A + size_t(gm) * lda + k0)
+                     : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < BC; ++i) {
+      const int gn = n0 + lr + 32 * i;
+      rb[i] = *reinterpret_cast<const uint4*>(W + size_t(gn) * ldw + k0);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < AC; ++i) {
+      const int r = lr + 32 * i;
+      sA[buf][r * 8 + (lc ^ (r & 7))] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < BC; ++i) {
+      const int r = lr + 32 * i;
+      sB[buf][r * 8 + (lc ^ (r & 7))] = rb[i];
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
+
+  const int KT = K / BK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  const int r32 = lane & 31, hi = lane >> 5;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) gload(kt + 1);
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int ch = kk * 2 + hi;
+      bf16x8 af[TM], bf[TN];
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int r = wm * WTM + a * 32 + r32;
+        af[a] = __builtin_bit_cast(bf16x8, sA[cur][r * 8 + (ch ^ (r & 7))]);
+      }
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int r = wn * WTN + b * 32 + r32;
+        bf[b] = __builtin_bit_cast(bf16x8, sB[cur][r * 8 + (ch ^ (r & 7))]);
+      }
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[b], acc[a][b], 0, 0, 0);
+    }
+    if (kt + 1 < KT) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // 32x32 accumulator layout: lane l, register i -> row 8(i/4) + 4(l/32) + i%4, column l%32.
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = m0 + wm * WTM + a * 32 + 8 * (i >> 2) + 4 * hi + (i & 3);
+        const int n = n0 + wn * WTN + b * 32 + r32;
+        if (m < M) epi(m, n, acc[a][b][i]);
+      }
+}
+
+template <int BM, int BN, int WM, int WN, class Epi>
+Status launch_bf16(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M, int N, int K,
+                   const Epi& epi, hipStream_t s) {
+  if (M <= 0) return Status::ok();
+  if (N % BN || K % 64) return Status::shape("bf16 GEMM needs N % tile == 0 and K % 64 == 0");
+  dim3 grid(N / BN, (M + BM - 1) / BM);
+  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, Epi>), grid, dim3(256), 0, s, A, lda, W, ldw, M,
+                     N, K, epi);
+  DC_HIP(hipGetLastError());
+  return Status::ok();
+}
+
+// ---------------------------------------------------------------------------
+// fp32 SIMT GEMM: 64x64 tile, k-step 16, each thread a 4x4 block of outputs
+// ---------------------------------------------------------------------------
+template <class Epi>
+__global__ void __launch_bounds__(256) k_gemm_f32(const float* __restrict__ A, int lda,
+                                                  const float* __restrict__ W, int ldw, int M,
+                                                  int N, int K, Epi epi) {
+  __shared__ float sA[16][64 + 4];
+  __shared__ float sW[16][64 + 4];
+  const int tid = threadIdx.x;
+  const int tx = tid & 15, ty = tid >> 4;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  const int lr = tid >> 2, lk = (tid & 3) * 4;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    const int gm = m0 + lr, gn = n0 + lr;
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f), w = a;
+    if (gm < M) a = *reinterpret_cast<const float4*>(A + size_t(gm) * lda + k0 + lk);
+    if (gn < N) w = *reinterpret_cast<const float4*>(W + size_t(gn) * ldw + k0 + lk);
+    sA[lk + 0][lr] = a.x; sA[lk + 1][lr] = a.y; sA[lk + 2][lr] = a.z; sA[lk + 3][lr] = a.w;
+    sW[lk + 0][lr] = w.x; sW[lk + 1][lr] = w.y; sW[lk + 2][lr] = w.z; sW[lk + 3][lr] = w.w;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      float av[4], wv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = sA[k][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) wv[j] = sW[k][tx + 16 * j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += av[i] * wv[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int m = m0 + ty * 4 + i, n = n0 + tx + 16 * j;
+      if (m < M && n < N) epi(m, n, acc[i][j]);
+    }
+}
+
+template <class Epi>
+Status launch_f32(const float* A, int lda, const float* W, int ldw, int M, int N, int K,
+                  const Epi& epi, hipStream_t s) {
+  if (M <= 0 || N <= 0) return Status::ok();
+  if (K % 16 || lda % 4 || ldw % 4) return Status::shape("f32 GEMM needs K % 16 == 0, aligned rows");
+  dim3 grid((N + 63) / 64, (M + 63) / 64);
+  hipLaunchKernelGGL(k_gemm_f32<Epi>, grid, dim3(256), 0, s, A, lda, W, ldw, M, N, K, epi);
+  DC_HIP(hipGetLastError());
+  return Status::ok();
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// entry points
+// ---------------------------------------------------------------------------
+Status gemm_f32_bias_act(const float* A, int lda, const float* W, int ldw, const float* bias,
+                         float* out, int ldo, int M, int N, int K, Act act, hipStream_t s) {
+  return launch_f32(A, lda, W, ldw, M, N, K, EpiBiasAct{bias, out, ldo, act == Act::kSilu ? 1 : 0}, s);
+}
+
+Status gemm_f32_gate_residual(const float* A, int lda, const float* W, int ldw, const float* bias,
+                              const float* gate, float* h, int ldh, int M, int N, int K,
+                              hipStream_t s) {
+  return launch_f32(A, lda, W, ldw, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
+}
+
+Status gemm_f32_gelu(const float* A, int lda, const float* W, int ldw, const float* bias,
+                     float* out, int ldo, int M, int N, int K, hipStream_t s) {
+  return launch_f32(A, lda, W, ldw, M, N, K, EpiGeluF32{bias, out, ldo}, s);
+}
+
+Status gemm_f32_patch_embed(const float* A, const float* W, const float* bias, const void* pos,
+                            bool pos_bf16, float* out, int ldo, int M, int N, hipStream_t s) {
+  EpiPatch e{bias, pos_bf16 ? nullptr : static_cast<const float*>(pos),
+             pos_bf16 ? static_cast<const uint16_t*>(pos) : nullptr, out, ldo};
+  return launch_f32(A, 64, W, 64, M, N, 64, e, s);
+}
+
+Status gemm_f32_head(const float* A, int lda, const float* W, const float* bias, float* x,
+                     float dsigma, const Geo& g, int M, hipStream_t s) {
+  EpiHeadEuler e{bias, x, dsigma, g.T, g.Hl, g.Wl, g.p, g.Hp, g.Wp};
+  return launch_f32(A, lda, W, g.d, M, g.P, g.d, e, s);
+}
+
+Status gemm_f32_qkv(const float* A, const float* W, const float* bias, float* qk, float* vt,
+                    int ldv, const Geo& g, int M, hipStream_t s) {
+  return launch_f32(A, g.d, W, g.d, M, 3 * g.d, g.d, EpiQKVF32{bias, qk, vt, g.d, ldv}, s);
+}
+
+Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, uint16_t* qk,
+                     uint16_t* vt, int ldv, const Geo& g, int M, hipStream_t s) {
+  return launch_bf16<256, 128, 2, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
+                                     EpiQKVBf16{bias, qk, vt, g.d, ldv}, s);
+}
+
+Status gemm_bf16_gate_residual(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
+                               const float* gate, float* h, int ldh, int M, int N, int K,
+                               hipStream_t s) {
+  return launch_bf16<256, 128, 2, 2>(A, lda, W, K, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
+}
+
+Status gemm_bf16_gelu(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
+                      uint16_t* out, int ldo, int M, int N, int K, hipStream_t s) {
+  return launch_bf16<256, 128, 2, 2>(A, lda, W, K, M, N, K, EpiGeluBf16{bias, out, ldo}, s);
+}
+
+Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float* bias, float* x,
+                      float dsigma, const Geo& g, int M, hipStream_t s) {
+  EpiHeadEuler e{bias, x, dsigma, g.T, g.Hl, g.Wl, g.p, g.Hp, g.Wp};
+  return launch_bf16<64, 64, 2, 2>(A, lda, W, g.d, M, g.P, g.d, e, s);
+}
+
+}  // namespace dc

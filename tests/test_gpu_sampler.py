@@ -1,0 +1,167 @@
+"""The whole cached sampler (dc_sampler / dc_denoise_step) against the oracle.
+
+Refresh/reuse masks must match bit-exactly; final latents within rel-L2 1e-4
+(fp32 model) and 2e-2 (bf16 model).  At full size, properties that hold at any
+size: masked batch dispatch equals single-scene runs bitwise, and a schedule
+whose every reuse is vetoed equals a scene outside the support (all refresh)."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import budget, dp, runtime
+from paper_2608_16354_amd import inputs as I
+from tests.gpu_util import rel_l2, say
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2608_16354_amd import api as A
+    A.L.load()
+    return A
+
+
+def run_gpu(api, dm, w, problems, x1, txt, steps=None, metric=0):
+    import torch
+    smp = api.Sampler(dm, problems, I.sigmas(w.K), torch.from_numpy(x1), torch.from_numpy(txt),
+                      drift_metric=metric)
+    rs, ds = [], []
+    for _ in range(w.K if steps is None else steps):
+        r, d = smp.step()
+        rs.append(r)
+        ds.append(d)
+    torch.cuda.synchronize()
+    x = smp.x.cpu().numpy()
+    plans = [smp.plan(b) for b in range(len(problems))]
+    smp.close()
+    return x, np.stack(rs), np.stack(ds), plans
+
+
+TINY = I.WORKLOADS["dit-tiny-f32"]
+
+
+@pytest.fixture(scope="module")
+def tiny_model(api, dev):
+    W = I.Weights(TINY.model, TINY.cfg_id)
+    return W, api.DeviceModel(W, dev)
+
+
+@pytest.mark.parametrize("thr", [I.NO_VETO, 0.0, 0.045])
+def test_tiny_fp32_sample_matches_oracle(api, tiny_model, thr):
+    W, dm = tiny_model
+    w = TINY
+    p = I.scene_problem(w, w.motions[0], thr=thr)
+    x1, txt = I.latent(w.model, 1, 0), I.text(w.model, 1, 0)
+    say("tiny sample thr", thr)
+    x, rs, ds, plans = run_gpu(api, dm, w, [p], x1[None], txt[None])
+    ref = runtime.sample(W, x1, txt, I.sigmas(w.K), p)
+    assert rs[:, 0].tolist() == ref.realized                          # bit-exact mask
+    assert plans[0][0].tolist() == ref.plan
+    assert plans[0][1] == sum(r.vetoed for r in ref.records)
+    for k, r in enumerate(ref.records):
+        if r.drift is None:
+            assert np.isnan(ds[k, 0])
+        else:
+            assert ds[k, 0] == pytest.approx(r.drift, rel=1e-4)
+            assert abs(ds[k, 0] - r.drift) < abs(r.drift - r.threshold)   # margin exceeds the error
+    err = rel_l2(x[0], ref.x)
+    say("tiny thr", thr, "final rel-L2", err, "mask", rs[:, 0].tolist())
+    assert err <= 1e-4
+
+
+def test_tiny_batch_masked_dispatch_matches_oracle_per_scene(api, tiny_model):
+    W, dm = tiny_model
+    w = TINY
+    motions = [I.Motion(8.0, 0.0), I.Motion(2.0, 0.1), I.Motion(15.0, -0.2), I.Motion(30.0, 0.0)]
+    probs = [I.scene_problem(w, m, thr=0.045) for m in motions]
+    x1 = np.stack([I.latent(w.model, 1, s) for s in range(4)])
+    txt = np.stack([I.text(w.model, 1, s) for s in range(4)])
+    say("tiny batch of 4")
+    x, rs, ds, _ = run_gpu(api, dm, w, probs, x1, txt)
+    for s in range(4):
+        ref = runtime.sample(W, x1[s], txt[s], I.sigmas(w.K), probs[s])
+        assert rs[:, s].tolist() == ref.realized
+        assert rel_l2(x[s], ref.x) <= 1e-4
+    assert rs[:, 3].sum() == 0                    # outside the support: full inference
+
+
+def test_tiny_veto_everything_equals_all_refresh(api, tiny_model):
+    w = TINY
+    _, dm = tiny_model
+    x1, txt = I.latent(w.model, 1, 0)[None], I.text(w.model, 1, 0)[None]
+    a = run_gpu(api, dm, w, [I.scene_problem(w, w.motions[0], thr=0.0)], x1, txt)
+    b = run_gpu(api, dm, w, [I.scene_problem(w, I.Motion(40.0, 0.0))], x1, txt)
+    assert a[1].sum() == 0 and b[1].sum() == 0
+    assert np.array_equal(a[0], b[0])
+
+
+def test_tiny_zero_residual_makes_caching_exact(api, dev):
+    w = TINY
+    Wz = I.Weights(w.model, w.cfg_id, zero_out=("w_o", "b_o", "w_2", "b_2"))
+    dm = api.DeviceModel(Wz, dev)
+    x1, txt = I.latent(w.model, 1, 0)[None], I.text(w.model, 1, 0)[None]
+    a = run_gpu(api, dm, w, [I.scene_problem(w, w.motions[0])], x1, txt)
+    b = run_gpu(api, dm, w, [I.scene_problem(w, w.motions[0], thr=0.0)], x1, txt)
+    assert a[1].sum() == 3 and b[1].sum() == 0
+    assert np.array_equal(a[0], b[0])
+
+
+def test_mid_bf16_sample_matches_stored_oracle(api, dev):
+    name = "dit-12x1152-bf16"
+    path = os.path.join(HERE, "golden", f"oracle_{name}.npz")
+    gold = np.load(path, allow_pickle=False)
+    import sys
+    sys.path.insert(0, os.path.join(HERE, "golden"))
+    from make_oracle_artifacts import fingerprint
+    w = I.WORKLOADS[name]
+    assert str(gold["fingerprint"]) == fingerprint(w), "input generator changed: regenerate the artefact"
+    cal = [I.scene_problem(w, m) for m in I.calibration_motions(32)]
+    tau = api.dc_select_tau(cal, w.rho)
+    assert tau == int(gold["tau_q"])
+    p = I.scene_problem(w, w.motions[0], tau_q=tau)
+    W = I.Weights(w.model, w.cfg_id)
+    say("upload", name)
+    dm = api.DeviceModel(W, dev)
+    x1, txt = I.latent(w.model, w.cfg_id, 0), I.text(w.model, w.cfg_id, 0)
+    say("sample", name)
+    x, rs, ds, _ = run_gpu(api, dm, w, [p], x1[None], txt[None])
+    assert rs[:, 0].tolist() == gold["realized"].tolist()
+    d = gold["drift"]
+    chk = ~np.isnan(d)
+    assert np.array_equal(np.isnan(ds[:, 0]), ~chk)
+    assert np.allclose(ds[chk, 0], d[chk], rtol=5e-2)
+    err = rel_l2(x[0], gold["x"])
+    say(name, "final rel-L2", err, "reuses", int(rs.sum()))
+    assert err <= 2e-2
+
+
+@pytest.mark.parametrize("name", ["dit-30x1920-bf16"])
+def test_full_size_schedule_and_batch_dispatch(api, dev, name):
+    """Full 17,776-token shape, first 6 steps: the sampler's plan is the oracle's
+    (bit-exact), and a batch of 4 scenes with different masks equals each scene
+    run alone, bitwise."""
+    w5 = I.WORKLOADS["dit-30x1920-bf16-b4"]
+    w = I.WORKLOADS[name]
+    cal = [I.scene_problem(w, m) for m in I.calibration_motions(32)]
+    tau = api.dc_select_tau(cal, w.rho)
+    assert tau == budget.select_tau(cal, w.rho)
+    probs = [I.scene_problem(w5, m, tau_q=tau) for m in I.scene_motions(w5)]
+    W = I.Weights(w.model, w.cfg_id)
+    say("upload", name)
+    dm = api.DeviceModel(W, dev)
+    x1 = np.stack([I.latent(w.model, w.cfg_id, s) for s in range(4)])
+    txt = np.stack([I.text(w.model, w.cfg_id, s) for s in range(4)])
+    steps = 6
+    say("batch of 4, steps", steps)
+    xb, rb, _, plans = run_gpu(api, dm, w5, probs, x1, txt, steps=steps)
+    for s in range(4):
+        assert plans[s][0].tolist() == dp.schedule(probs[s]).reuse
+    assert len({tuple(rb[:, s]) for s in range(4)}) > 1           # masks differ across scenes
+    for s in range(4):
+        say("scene alone", s)
+        xs, rs, _, _ = run_gpu(api, dm, w5, [probs[s]], x1[s:s + 1], txt[s:s + 1], steps=steps)
+        assert rs[:, 0].tolist() == rb[:, s].tolist()
+        assert np.array_equal(xs[0], xb[s])
