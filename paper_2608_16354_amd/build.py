@@ -23,6 +23,8 @@ ARCH = "gfx950"
 HIPCC_FLAGS = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                "-ffp-contract=fast", "-Wall", "-Wno-unused-result"]
+# per-file extra flags: keep MFMA accumulators in VGPRs where the softmax reads them
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=true"]}
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-ffp-contract=off", "-D__HIP_PLATFORM_AMD__",
               f"-I{ROCM}/include", "-Wall"]
 
@@ -49,7 +51,7 @@ def build(verbose: bool = False) -> str:
         obj = os.path.join(BUILD, f + ".o")
         objs.append(obj)
         if f.endswith(".hip"):
-            jobs.append([hipcc, *HIPCC_FLAGS, "-c", src, "-o", obj])
+            jobs.append([hipcc, *HIPCC_FLAGS, *EXTRA_FLAGS.get(f, []), "-c", src, "-o", obj])
         else:
             jobs.append([clang, *HOST_FLAGS, "-c", src, "-o", obj])
     with ThreadPoolExecutor(max(1, min(8, os.cpu_count() or 1))) as ex:

@@ -29,11 +29,15 @@ __device__ inline uint16_t to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
-// LDS chunk swizzles.  K tile rows are read in the permuted order
-// {0,1,2,3,8,9,10,11} by 8 consecutive lanes: key the swizzle on row bits 0,1,3.
-__device__ inline int swz_k(int row) { return (row & 3) | (((row >> 3) & 1) << 2); }
-__device__ inline int swz_v(int row) { return row & 7; }
+// LDS chunk swizzle for 128-byte tile rows.  gfx950's LDS serves 256 bytes per
+// cycle (64 banks): two consecutive rows share a bank cycle, so the XOR key is
+// row / 2, which gives the 16 rows that 16 consecutive lanes read (in any order,
+// including the permuted K order) 16 distinct 16-byte bank groups.
+__device__ inline int swz_k(int row) { return (row >> 1) & 7; }
+__device__ inline int swz_v(int row) { return (row >> 1) & 7; }
 __device__ inline int perm_kv(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
+
+constexpr float kSlack = 8.0f;   // lazy-rescale threshold of the running max (log2 units)
 
 template <int D>
 __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ qk,
@@ -180,24 +184,30 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mnew = fmaxf(mrow, mx * scale_log2);
-    const float alpha = __builtin_amdgcn_exp2f(mrow - mnew);
-    mrow = mnew;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
+    // Lazy rescale: keep the running max unless some row of the wave grows by
+    // more than kSlack (log2 units); stale maxima only scale P and the row sum
+    // by at most 2^kSlack, which fp32 accumulation absorbs.
+    if (__builtin_amdgcn_ballot_w64(mx > mrow + kSlack) != 0) {
+      const float mnew = fmaxf(mrow, mx);
+      const float alpha = __builtin_amdgcn_exp2f(mrow - mnew);
+      mrow = mnew;
+      lsum *= alpha;
+#pragma unroll
+      for (int tv = 0; tv < TV; ++tv)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[tv][i] *= alpha;
+    }
     float ps = 0.f;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float pv = __builtin_amdgcn_exp2f(s[st][i] * scale_log2 - mnew);
+        const float pv = __builtin_amdgcn_exp2f(s[st][i] * scale_log2 - mrow);
         s[st][i] = pv;
         ps += pv;
       }
-    lsum = lsum * alpha + ps;
-#pragma unroll
-    for (int tv = 0; tv < TV; ++tv)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) o[tv][i] *= alpha;
+    lsum += ps;
 
     // O^T += V^T P^T over the four 16-token slices of the tile
 #pragma unroll

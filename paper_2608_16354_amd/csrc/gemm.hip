@@ -2,8 +2,7 @@
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 tiles (gfx950), 256 threads = 4 waves,
 // block tile BM x BN x 64, double-buffered LDS with an XOR swizzle on the 16-byte
-// chunks of each 128-byte row (so the 8 rows read by 8 consecutive lanes hit 8
-// different chunks), one barrier per k-step, the next k-tile prefetched into
+// chunks of each 128-byte row (conflict-free reads of 16 rows by 16 lanes), one barrier per k-step, the next k-tile prefetched into
 // registers while the current one is multiplied.
 // f32 path: a plain SIMT tiled kernel for the fp32 model and the small
 // fp32 GEMMs (patch embedding, timestep MLP).
@@ -22,6 +21,12 @@ __device__ inline uint16_t to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 __device__ inline float from_bf16(uint16_t u) { return __uint_as_float(uint32_t(u) << 16); }
+
+// LDS chunk swizzle for 128-byte tile rows.  gfx950's LDS serves 256 bytes per
+// cycle (64 banks), so two consecutive 128-byte rows share a bank cycle: keying
+// the XOR on row / 2 makes the 16 rows read by 16 consecutive lanes hit 16
+// distinct 16-byte bank groups.
+__device__ inline int swz(int row) { return (row >> 1) & 7; }
 
 // GELU with the tanh approximation, written as z * sigmoid(2y), y = sqrt(2/pi)(z + 0.044715 z^3)
 // (0.5 (1 + tanh y) = 1 / (1 + exp(-2y))).
@@ -135,12 +140,12 @@ __global__ void __launch_bounds__(256) k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
     for (int i = 0; i < AC; ++i) {
       const int r = lr + 32 * i;
-      sA[buf][r * 8 + (lc ^ (r & 7))] = ra[i];
+      sA[buf][r * 8 + (lc ^ swz(r))] = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < BC; ++i) {
       const int r = lr + 32 * i;
-      sB[buf][r * 8 + (lc ^ (r & 7))] = rb[i];
+      sB[buf][r * 8 + (lc ^ swz(r))] = rb[i];
     }
   };
 
@@ -167,12 +172,12 @@ __global__ void __launch_bounds__(256) k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
       for (int a = 0; a < TM; ++a) {
         const int r = wm * WTM + a * 32 + r32;
-        af[a] = __builtin_bit_cast(bf16x8, sA[cur][r * 8 + (ch ^ (r & 7))]);
+        af[a] = __builtin_bit_cast(bf16x8, sA[cur][r * 8 + (ch ^ swz(r))]);
       }
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int r = wn * WTN + b * 32 + r32;
-        bf[b] = __builtin_bit_cast(bf16x8, sB[cur][r * 8 + (ch ^ (r & 7))]);
+        bf[b] = __builtin_bit_cast(bf16x8, sB[cur][r * 8 + (ch ^ swz(r))]);
       }
 #pragma unroll
       for (int a = 0; a < TM; ++a)
@@ -195,6 +200,140 @@ __global__ void __launch_bounds__(256) k_gemm_bf16(const uint16_t* __restrict__ 
         const int n = n0 + wn * WTN + b * 32 + r32;
         if (m < M) epi(m, n, acc[a][b][i]);
       }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM, LDS-DMA pipeline.  512 threads = 8 waves (2 per SIMD), block
+// tile BM x BN x 64.  Tiles go global -> LDS with global_load_lds_dwordx4 (lane i
+// of an instruction lands at LDS base + 16 i, so the XOR swizzle is applied to the
+// global address each lane fetches): no staging registers and no LDS write
+// instructions.  Two stages in separate LDS arrays (so the compiler can tell
+// them apart and does not drain every load before each LDS read), one barrier
+// per k-step: the loads for step k+1 are issued right after it and overlap the
+// MFMAs of step k.  Rows past M or N are clamped to the last row (their results
+// are never stored).  Workgroups are renumbered so that each XCD (assigned
+// round-robin by workgroup id) processes a contiguous range of tiles.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int BM, int BN, int WM, int WN, class Epi>
+__global__ void __launch_bounds__(512) k_gemm_dma(const uint16_t* __restrict__ A, int lda,
+                                                  const uint16_t* __restrict__ W, int ldw, int M,
+                                                  int N, int K, int tiles_n, int tiles, int per_xcd,
+                                                  Epi epi) {
+  constexpr int BK = 64;
+  constexpr int NW = WM * WN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int AI = BM * 8 / 64 / NW, BI = BN * 8 / 64 / NW;   // DMA instructions per wave
+  static_assert(NW == 8 && TM >= 1 && TN >= 1 && AI * NW * 64 == BM * 8 && BI * NW * 64 == BN * 8,
+                "tile shape");
+  __shared__ uint4 sA0[BM * 8], sA1[BM * 8];
+  __shared__ uint4 sB0[BN * 8], sB1[BN * 8];
+
+  const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (t >= tiles) return;
+  const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+
+  // per-lane global element offsets of this wave's DMA instructions (k-step 0)
+  size_t offA[AI], offB[BI];
+#pragma unroll
+  for (int i = 0; i < AI; ++i) {
+    const int slot = (wave * AI + i) * 64 + lane;
+    const int r = slot >> 3, c = (slot & 7) ^ swz(slot >> 3);
+    offA[i] = size_t(min(m0 + r, M - 1)) * lda + 8 * c;
+  }
+#pragma unroll
+  for (int i = 0; i < BI; ++i) {
+    const int slot = (wave * BI + i) * 64 + lane;
+    const int r = slot >> 3, c = (slot & 7) ^ swz(slot >> 3);
+    offB[i] = size_t(min(n0 + r, N - 1)) * ldw + 8 * c;
+  }
+  auto issue = [&](uint4* sa, uint4* sb, int kt) {
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int i = 0; i < AI; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(A + offA[i] + k0),
+                                       (lds_void*)(sa + (wave * AI + i) * 64), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < BI; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(W + offB[i] + k0),
+                                       (lds_void*)(sb + (wave * BI + i) * 64), 16, 0, 0);
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
+
+  const int r32 = lane & 31, hi = lane >> 5;
+  auto compute = [&](const uint4* sa, const uint4* sb) {
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int ch = kk * 2 + hi;
+      bf16x8 af[TM], bf[TN];
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int r = wm * WTM + a * 32 + r32;
+        af[a] = __builtin_bit_cast(bf16x8, sa[r * 8 + (ch ^ swz(r))]);
+      }
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int r = wn * WTN + b * 32 + r32;
+        bf[b] = __builtin_bit_cast(bf16x8, sb[r * 8 + (ch ^ swz(r))]);
+      }
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[b], acc[a][b], 0, 0, 0);
+    }
+  };
+
+  const int KT = K / BK;
+  issue(sA0, sB0, 0);
+  for (int kt = 0; kt < KT; kt += 2) {
+    // stage 0 holds k-step kt
+    __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave's loads landed
+    __builtin_amdgcn_s_barrier();                // everyone's landed; stage 1 is free
+    if (kt + 1 < KT) issue(sA1, sB1, kt + 1);
+    compute(sA0, sB0);
+    if (kt + 1 >= KT) break;
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_s_barrier();                // stage 0 is free
+    if (kt + 2 < KT) issue(sA0, sB0, kt + 2);
+    compute(sA1, sB1);
+  }
+
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = m0 + wm * WTM + a * 32 + 8 * (i >> 2) + 4 * hi + (i & 3);
+        const int n = n0 + wn * WTN + b * 32 + r32;
+        if (m < M && n < N) epi(m, n, acc[a][b][i]);
+      }
+}
+
+template <int BM, int BN, int WM, int WN, class Epi>
+Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M, int N, int K,
+                  const Epi& epi, hipStream_t s) {
+  if (M <= 0) return Status::ok();
+  if (K % 64 || lda % 8 || ldw % 8) return Status::shape("bf16 GEMM needs K % 64 == 0 and 16-byte rows");
+  const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
+  const int tiles = tn * tm;
+  const int per = (tiles + 7) / 8;
+  hipLaunchKernelGGL((k_gemm_dma<BM, BN, WM, WN, Epi>), dim3(8 * per), dim3(512), 0, s, A, lda, W,
+                     ldw, M, N, K, tn, tiles, per, epi);
+  DC_HIP(hipGetLastError());
+  return Status::ok();
 }
 
 template <int BM, int BN, int WM, int WN, class Epi>
@@ -306,19 +445,19 @@ Status gemm_f32_qkv(const float* A, const float* W, const float* bias, float* qk
 
 Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, uint16_t* qk,
                      uint16_t* vt, int ldv, const Geo& g, int M, hipStream_t s) {
-  return launch_bf16<256, 128, 2, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
-                                     EpiQKVBf16{bias, qk, vt, g.d, ldv}, s);
+  return launch_dma<256, 192, 4, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
+                                    EpiQKVBf16{bias, qk, vt, g.d, ldv}, s);
 }
 
 Status gemm_bf16_gate_residual(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
                                const float* gate, float* h, int ldh, int M, int N, int K,
                                hipStream_t s) {
-  return launch_bf16<256, 128, 2, 2>(A, lda, W, K, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
+  return launch_dma<256, 192, 4, 2>(A, lda, W, K, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
 }
 
 Status gemm_bf16_gelu(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
                       uint16_t* out, int ldo, int M, int N, int K, hipStream_t s) {
-  return launch_bf16<256, 128, 2, 2>(A, lda, W, K, M, N, K, EpiGeluBf16{bias, out, ldo}, s);
+  return launch_dma<256, 192, 4, 2>(A, lda, W, K, M, N, K, EpiGeluBf16{bias, out, ldo}, s);
 }
 
 Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float* bias, float* x,
