@@ -39,21 +39,39 @@ __device__ inline int perm_kv(int m) { return (m & ~12) | ((m & 4) << 1) | ((m &
 
 constexpr float kSlack = 8.0f;   // lazy-rescale threshold of the running max (log2 units)
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int D>
+struct AttnShape {
+  static constexpr int DK = (D + 15) / 16 * 16;   // contraction width of Q K^T (zero padded)
+  static constexpr int KC = DK / 8;               // 16-byte chunks per K row in LDS
+  static constexpr int DC8 = D / 8;               // chunks holding real data
+  static constexpr int DV = (D + 31) / 32 * 32;   // rows of the O^T accumulator
+  static constexpr int TV = DV / 32;
+  static constexpr int BKV = 64;                  // tokens per K/V tile
+  static constexpr int KSLOTS = BKV * KC;         // 16-byte LDS slots of a K tile
+  static constexpr int VSLOTS = DV * 8;           // of a V^T tile (64 tokens = 8 chunks per row)
+  static constexpr int KI = (KSLOTS + 255) / 256; // DMA instructions per wave (4 waves x 64 lanes)
+  static constexpr int VI = (VSLOTS + 255) / 256;
+};
+
+// K/V^T tiles go global -> LDS with global_load_lds_dwordx4 into a ring of three
+// stages (separate arrays), prefetched two tiles ahead; one barrier per tile.
+// Lane i of a DMA instruction lands at the instruction's LDS base + 16 i, so each
+// lane fetches the global chunk that belongs at its slot: the swizzle and the
+// K-padding are applied on the global side.  Rows past the data (K rows past M,
+// padding chunks, V^T rows past D) fetch real, finite data whose products are
+// either multiplied by zero (padded Q columns, masked P) or never stored.
 template <int D>
 __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ qk,
                                                    const uint16_t* __restrict__ vt, int ldv,
                                                    uint16_t* __restrict__ out, int M, int d,
                                                    float scale_log2) {
-  constexpr int DK = (D + 15) / 16 * 16;   // contraction width of Q K^T (zero padded)
-  constexpr int KC = DK / 8;               // 16-byte chunks per K row
-  constexpr int DC8 = D / 8;               // chunks holding real data
-  constexpr int DV = (D + 31) / 32 * 32;   // rows of the O^T accumulator
-  constexpr int TV = DV / 32;
-  constexpr int BKV = 64;
-  constexpr int KLD = (BKV * DC8 + 255) / 256;   // K chunks per thread per tile
-  constexpr int VLD = (D * 8 + 255) / 256;       // V^T chunks per thread per tile
-  __shared__ uint4 sK[2][BKV * KC];
-  __shared__ uint4 sV[2][DV * 8];
+  using S = AttnShape<D>;
+  constexpr int DK = S::DK, KC = S::KC, DC8 = S::DC8, TV = S::TV, BKV = S::BKV;
+  constexpr int KI = S::KI, VI = S::VI;
+  __shared__ uint4 sK0[KI * 256], sK1[KI * 256], sK2[KI * 256];
+  __shared__ uint4 sV0[VI * 256], sV1[VI * 256], sV2[VI * 256];
 
   const int head = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -64,19 +82,6 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   const uint16_t* Kb = qk + d + head * D;
   const uint16_t* Vb = vt + size_t(head) * D * ldv;
   const uint4 zero4 = make_uint4(0, 0, 0, 0);
-
-  // zero the padding that loads never write: K chunks past D, V^T rows past D
-  if constexpr (KC > DC8) {
-    for (int e = tid; e < BKV * (KC - DC8); e += 256) {
-      const int r = e / (KC - DC8), c = DC8 + e % (KC - DC8);
-      sK[0][r * KC + c] = zero4;
-      sK[1][r * KC + c] = zero4;
-    }
-  }
-  for (int e = tid; e < (DV - D) * 8; e += 256) {
-    sV[0][D * 8 + e] = zero4;
-    sV[1][D * 8 + e] = zero4;
-  }
 
   // query fragments (B operand of S^T): lane holds Q[q0 + r32][16 kk + 8 g .. + 8]
   bf16x8 qf[DK / 16];
@@ -89,54 +94,39 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     qf[kk] = __builtin_bit_cast(bf16x8, v);
   }
 
-  uint4 rk[KLD], rv[VLD];
-  auto gload = [&](int t) {
+  // per-lane source offsets of this wave's DMA instructions for tile 0
+  size_t offK[KI];
+  int offV[VI];
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const int slot = (wave * KI + i) * 64 + lane;
+    const int r = slot / KC, pc = slot % KC;
+    const int c = (KC == 8) ? (pc ^ swz_k(r)) : pc;
+    const int cc = c < DC8 ? c : 0;                    // padding chunk: any real chunk
+    offK[i] = size_t(min(r, M - 1)) * ldq + 8 * cc;   // tile-relative row r, clamped below
+  }
+#pragma unroll
+  for (int i = 0; i < VI; ++i) {
+    const int slot = (wave * VI + i) * 64 + lane;
+    const int r = slot >> 3, c = (slot & 7) ^ swz_v(slot >> 3);
+    offV[i] = min(r, D - 1) * ldv + 8 * c;
+  }
+  auto issue = [&](uint4* sk, uint4* sv, int t) {
     const int kv0 = t * BKV;
 #pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      const int e = tid + 256 * i;
-      rk[i] = zero4;
-      if (e < BKV * DC8) {
-        const int r = e / DC8, c = e % DC8;
-        if (kv0 + r < M) rk[i] = *reinterpret_cast<const uint4*>(Kb + size_t(kv0 + r) * ldq + 8 * c);
-      }
+    for (int i = 0; i < KI; ++i) {
+      const int slot = (wave * KI + i) * 64 + lane;
+      const int r = slot / KC;
+      // clamp the token to the last one (rows past M are masked out of the softmax)
+      const size_t rowfix = (kv0 + r < M) ? size_t(kv0) * ldq
+                                          : size_t(M - 1 - min(r, M - 1)) * ldq;
+      __builtin_amdgcn_global_load_lds((const void*)(Kb + offK[i] + rowfix),
+                                       (lds_void*)(sk + (wave * KI + i) * 64), 16, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < VLD; ++i) {
-      const int e = tid + 256 * i;
-      rv[i] = zero4;
-      if (e < D * 8) {
-        const int r = e >> 3, c = e & 7;
-        const int kv = kv0 + 8 * c;
-        if (kv < M) {
-          uint4 v = *reinterpret_cast<const uint4*>(Vb + size_t(r) * ldv + kv);
-          if (kv + 8 > M) {   // ragged tail: zero the tokens past M
-            uint16_t* h = reinterpret_cast<uint16_t*>(&v);
-            for (int j = M - kv; j < 8; ++j) h[j] = 0;
-          }
-          rv[i] = v;
-        }
-      }
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      const int e = tid + 256 * i;
-      if (e < BKV * DC8) {
-        const int r = e / DC8, c = e % DC8;
-        const int pc = (KC == 8) ? (c ^ swz_k(r)) : c;
-        sK[buf][r * KC + pc] = rk[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VLD; ++i) {
-      const int e = tid + 256 * i;
-      if (e < D * 8) {
-        const int r = e >> 3, c = e & 7;
-        sV[buf][r * 8 + (c ^ swz_v(r))] = rv[i];
-      }
-    }
+    for (int i = 0; i < VI; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(Vb + offV[i] + kv0),
+                                       (lds_void*)(sv + (wave * VI + i) * 64), 16, 0, 0);
   };
 
   f32x16 o[TV];
@@ -146,14 +136,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     for (int i = 0; i < 16; ++i) o[t][i] = 0.f;
   float mrow = -INFINITY, lsum = 0.f;
 
-  const int nkv = (M + BKV - 1) / BKV;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int t = 0; t < nkv; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < nkv) gload(t + 1);
-
+  auto compute = [&](const uint4* sk, const uint4* sv, int t) {
     // S^T for two 32-token sub-tiles; sub-tile st, register i holds token
     // 32 st + 16 (i / 8) + 8 g + (i % 8) of the tile, query q0 + r32.
     f32x16 s[2];
@@ -166,7 +149,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
       for (int kk = 0; kk < DK / 16; ++kk) {
         const int ch = 2 * kk + g;
         const int pc = (KC == 8) ? (ch ^ swz_k(row)) : ch;
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, sK[cur][row * KC + pc]);
+        const bf16x8 kf = __builtin_bit_cast(bf16x8, sk[row * KC + pc]);
         s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[st], 0, 0, 0);
       }
     }
@@ -208,7 +191,6 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
         ps += pv;
       }
     lsum += ps;
-
     // O^T += V^T P^T over the four 16-token slices of the tile
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -219,12 +201,30 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
 #pragma unroll
       for (int tv = 0; tv < TV; ++tv) {
         const int row = 32 * tv + r32;
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, sV[cur][row * 8 + (ch ^ swz_v(row))]);
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, sv[row * 8 + (ch ^ swz_v(row))]);
         o[tv] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[tv], 0, 0, 0);
       }
     }
-    if (t + 1 < nkv) sstore(cur ^ 1);
-    __syncthreads();
+  };
+
+  // vmcnt(n) with the other counters left alone
+  constexpr int kPerTile = KI + VI;
+  const int nkv = (M + BKV - 1) / BKV;
+  issue(sK0, sV0, 0);
+  if (nkv > 1) issue(sK1, sV1, 1);
+  auto step = [&](uint4* sk, uint4* sv, uint4* nk, uint4* nv, int t) {
+    if (t + 1 < nkv) __builtin_amdgcn_s_waitcnt(0x0F70 | kPerTile);   // tile t landed (t+1 may fly)
+    else __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_s_barrier();          // everyone's tile t landed; tile t-1's stage is free
+    if (t + 2 < nkv) issue(nk, nv, t + 2);
+    compute(sk, sv, t);
+  };
+  for (int t = 0; t < nkv; t += 3) {
+    step(sK0, sV0, sK2, sV2, t);
+    if (t + 1 >= nkv) break;
+    step(sK1, sV1, sK0, sV0, t + 1);
+    if (t + 2 >= nkv) break;
+    step(sK2, sV2, sK1, sV1, t + 2);
   }
 
   lsum += __shfl_xor(lsum, 32, 64);
@@ -247,6 +247,15 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
         }
       }
   }
+}
+
+// Zero the padding columns [M, ldv) of the transposed values (never written by
+// the QKV GEMM; the attention DMA reads them and multiplies them by zero).
+__global__ void k_zero_vt_tail(uint16_t* vt, int rows, int ldv, int M) {
+  const int w = ldv - M;
+  const size_t n = size_t(rows) * w;
+  for (size_t e = size_t(blockIdx.x) * blockDim.x + threadIdx.x; e < n; e += size_t(gridDim.x) * blockDim.x)
+    vt[(e / w) * ldv + M + (e % w)] = 0;
 }
 
 // fp32 path: one thread per query row, key/value tiles of 64 tokens in LDS.
@@ -296,6 +305,12 @@ __global__ void __launch_bounds__(64) k_attn_f32(const float* __restrict__ qk,
 
 Status attention_bf16(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t* out,
                       const Geo& g, int M, hipStream_t s) {
+  if (ldv % 64 || ldv < M) return Status::shape("attention needs ldv >= M, ldv % 64 == 0");
+  if (ldv > M) {
+    uint16_t* v = const_cast<uint16_t*>(vt);
+    hipLaunchKernelGGL(k_zero_vt_tail, dim3(64), dim3(256), 0, s, v, g.d, ldv, M);
+    DC_HIP(hipGetLastError());
+  }
   const float scale_log2 = float(1.4426950408889634 / std::sqrt(double(g.Dh)));
   dim3 grid((M + 127) / 128, g.H);
   if (g.Dh == 64)
