@@ -69,7 +69,7 @@ Workspace workspace_layout(const Geo& g, int batch) {
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
   w.a = take(size_t(g.N) * g.d * g.esz);
-  w.qk = take(size_t(g.N) * 2 * g.d * g.esz);
+  w.qk = take(size_t(w.ldv + 64) * 2 * g.d * g.esz);   // padding rows for the attention's K tiles
   w.vt = take(size_t(g.d) * w.ldv * g.esz);
   w.o = take(size_t(g.N) * g.d * g.esz);
   w.ff = take(size_t(g.N) * g.F * g.esz);

@@ -94,16 +94,18 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     qf[kk] = __builtin_bit_cast(bf16x8, v);
   }
 
-  // per-lane source offsets of this wave's DMA instructions for tile 0
-  size_t offK[KI];
-  int offV[VI];
+  // per-lane source offsets of this wave's DMA instructions for tile 0; tile t
+  // adds a uniform t * 64 rows (K) or t * 64 columns (V^T).  K rows run up to
+  // 64 + 12 past the tile start: the qk buffer has ldv + 64 rows, and rows past M
+  // only feed scores that the last tile masks (by assignment, so any bits are safe).
+  int offK[KI], offV[VI];
 #pragma unroll
   for (int i = 0; i < KI; ++i) {
     const int slot = (wave * KI + i) * 64 + lane;
     const int r = slot / KC, pc = slot % KC;
     const int c = (KC == 8) ? (pc ^ swz_k(r)) : pc;
     const int cc = c < DC8 ? c : 0;                    // padding chunk: any real chunk
-    offK[i] = size_t(min(r, M - 1)) * ldq + 8 * cc;   // tile-relative row r, clamped below
+    offK[i] = r * ldq + 8 * cc;
   }
 #pragma unroll
   for (int i = 0; i < VI; ++i) {
@@ -112,20 +114,15 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     offV[i] = min(r, D - 1) * ldv + 8 * c;
   }
   auto issue = [&](uint4* sk, uint4* sv, int t) {
-    const int kv0 = t * BKV;
+    const uint16_t* kt = Kb + size_t(t) * BKV * ldq;
+    const uint16_t* vtt = Vb + t * BKV;
 #pragma unroll
-    for (int i = 0; i < KI; ++i) {
-      const int slot = (wave * KI + i) * 64 + lane;
-      const int r = slot / KC;
-      // clamp the token to the last one (rows past M are masked out of the softmax)
-      const size_t rowfix = (kv0 + r < M) ? size_t(kv0) * ldq
-                                          : size_t(M - 1 - min(r, M - 1)) * ldq;
-      __builtin_amdgcn_global_load_lds((const void*)(Kb + offK[i] + rowfix),
+    for (int i = 0; i < KI; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(kt + offK[i]),
                                        (lds_void*)(sk + (wave * KI + i) * 64), 16, 0, 0);
-    }
 #pragma unroll
     for (int i = 0; i < VI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(Vb + offV[i] + kv0),
+      __builtin_amdgcn_global_load_lds((const void*)(vtt + offV[i]),
                                        (lds_void*)(sv + (wave * VI + i) * 64), 16, 0, 0);
   };
 
