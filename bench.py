@@ -22,6 +22,27 @@ sys.path.insert(0, ROOT)
 
 MI355X_BF16_DENSE_TFLOPS = 2500.0     # published dense bf16 MFMA peak
 MI355X_HBM_GBPS = 8000.0
+COPY_BYTES = 1 << 30                  # plain device copy used to scale the HBM byte counters
+
+
+def traffic_from_profile(kernel_file):
+    """HBM bytes per launch of the dominant kernel from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE per dispatch, scaled by a plain copy of known size),
+    or None when the kernel source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "attention_dit-30x1920-bf16_traffic.txt")
+    src = os.path.join(ROOT, "paper_2608_16354_amd", "csrc", kernel_file)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if kv.get("source_sha256") != sha:
+        return None
+    return float(kv["hbm_bytes_per_launch"])
 
 
 def log(*a):
@@ -91,6 +112,8 @@ def main():
     ap.add_argument("--workload", default="dit-30x1920-bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the live kernel timing")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -106,6 +129,14 @@ def main():
     w = I.WORKLOADS[args.workload]
     m = w.model
     dev = "cuda:0"
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"copy calibration: 3 x {COPY_BYTES} B device copies")
     t0 = time.time()
     W = I.Weights(m, w.cfg_id)
     dm = api.DeviceModel(W, dev)
@@ -167,7 +198,8 @@ def main():
         achieved = attention_flops(m) / (avg_ms / 1000.0) / 1e12
         out["roofline"] = {"kernel": "attention", "bound": "mfma", "achieved": achieved,
                            "peak": MI355X_BF16_DENSE_TFLOPS, "unit": "TFLOP/s",
-                           "frac": achieved / MI355X_BF16_DENSE_TFLOPS, "traffic": None,
+                           "frac": achieved / MI355X_BF16_DENSE_TFLOPS,
+                           "traffic": traffic_from_profile("attention.hip"),
                            "launches": n, "avg_ms": avg_ms}
     # refresh FLOPs of the executed schedule over the whole sample time (reuse steps included)
     out["sample_tflops"] = refresh_flops(m) * n_refresh / (ms_per / 1000.0) / 1e12
