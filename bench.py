@@ -63,7 +63,7 @@ def refresh_flops(m):
 
 def cpu_baseline(w, W, schedule, budget_s=30.0):
     """The fp64 oracle on a bounded sample of the same workload, extrapolated to one
-    cached sample: one block at full length on two query-row subsets (the per-block
+    cached sample: one block at full length on two query-row subsets (1024 and 4096 rows) (the per-block
     cost is fixed key/value work plus a per-row cost) and one full reuse step."""
     import numpy as np
     from oracle import dit
@@ -75,13 +75,13 @@ def cpu_baseline(w, W, schedule, budget_s=30.0):
     h = I.hidden_state(m, (90,)).astype(np.float64)
     rng = np.random.default_rng(0)
     times = {}
-    for R in (128, 512):
+    for R in (1024, 4096):
         rows = np.sort(rng.choice(m.n_tok, R, replace=False))
         t0 = time.perf_counter()
         dit.block(P, 0, mods[0], h, rows=rows)
         times[R] = time.perf_counter() - t0
-    per_row = (times[512] - times[128]) / (512 - 128)
-    fixed = max(times[128] - 128 * per_row, 0.0)
+    per_row = (times[4096] - times[1024]) / (4096 - 1024)
+    fixed = max(times[1024] - 1024 * per_row, 0.0)
     t_block = fixed + m.n_tok * per_row
     x = I.latent(m, w.cfg_id, 0).astype(np.float64)
     txt = I.text(m, w.cfg_id, 0)
@@ -99,8 +99,8 @@ def cpu_baseline(w, W, schedule, budget_s=30.0):
     spent = sum(times.values()) + t_reuse
     return {"value": w.batch * m.n_v * w.K / (w.batch * t_sample), "unit": "latent token*steps/s",
             "cores": cores, "kind": "oracle",
-            "sample": (f"fp64 oracle: one block at {m.n_tok} tokens on 128 and 512 query rows "
-                       f"({times[128]:.1f}s, {times[512]:.1f}s) + one full reuse step ({t_reuse:.1f}s), "
+            "sample": (f"fp64 oracle: one block at {m.n_tok} tokens on 1024 and 4096 query rows "
+                       f"({times[1024]:.1f}s, {times[4096]:.1f}s) + one full reuse step ({t_reuse:.1f}s), "
                        f"extrapolated to the {n_ref}-refresh/{n_reu}-reuse schedule; {spent:.0f}s of CPU work")}
 
 

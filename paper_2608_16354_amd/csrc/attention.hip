@@ -2,7 +2,9 @@
 // an online softmax (flash-style: the N x N score matrix never leaves registers).
 //
 // bf16 path (gfx950 MFMA 32x32x16).  A workgroup is 4 waves x 32 query rows of one
-// head; key/value tiles of 64 tokens are double-buffered in LDS.  Each wave
+// head; key/value tiles of 64 tokens stream through a 3-stage LDS ring.  The QKV
+// GEMM stores Q pre-multiplied by log2(e)/sqrt(d_h), so scores arrive in log2
+// units and P = 2^(s - m).  Each wave
 // computes the transposed scores S^T = K Q^T, so in the accumulator layout every
 // lane holds scores of a single query row (lane % 32): the row max needs one
 // cross-lane exchange (lanes l and l^32) and the rescale of the output is a
@@ -12,6 +14,11 @@
 // swapped) so that the eight scores a lane holds for each 16-token slice of P are
 // eight consecutive tokens: P goes from the score registers straight into the
 // B operand of the P V product, and V^T is read with one 16-byte LDS load.
+// Per-score VALU work is kept to the exponential, the bf16 conversion, a share of
+// a v_max3 and of a v_dot2 (the row sum adds pairs of bf16 P values): the
+// subtraction of the running maximum m rides on the MFMA as one extra rank-1
+// step (a column of ones times -m), and m is only raised when a score exceeds it
+// by more than a slack (lazy rescale).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -41,6 +48,19 @@ constexpr float kSlack = 8.0f;   // lazy-rescale threshold of the running max (l
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// 16 bytes per lane global -> LDS (global_load_lds_dwordx4): lane i's bytes land
+// at the wave-uniform LDS address dst + 16 i.  Issued as inline assembly: the
+// compiler cannot tell the stage being filled from the stage being read and
+// would otherwise wait for every outstanding fill before each LDS read.  The
+// kernel waits for its own fills explicitly (vmcnt) before the barrier that
+// publishes a stage.
+__device__ inline void dma16(const void* src, const void* dst) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst)));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(lds) : "memory", "m0");
+}
+
 template <int D>
 struct AttnShape {
   static constexpr int DK = (D + 15) / 16 * 16;   // contraction width of Q K^T (zero padded)
@@ -55,8 +75,8 @@ struct AttnShape {
   static constexpr int VI = (VSLOTS + 255) / 256;
 };
 
-// K/V^T tiles go global -> LDS with global_load_lds_dwordx4 into a ring of three
-// stages (separate arrays), prefetched two tiles ahead; one barrier per tile.
+// K/V^T tiles go global -> LDS into a ring of three stages (separate arrays),
+// prefetched two tiles ahead; one barrier per tile.
 // Lane i of a DMA instruction lands at the instruction's LDS base + 16 i, so each
 // lane fetches the global chunk that belongs at its slot: the swizzle and the
 // K-padding are applied on the global side.  Rows past the data (K rows past M,
@@ -66,17 +86,23 @@ template <int D>
 __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ qk,
                                                    const uint16_t* __restrict__ vt, int ldv,
                                                    uint16_t* __restrict__ out, int M, int d,
-                                                   float scale_log2) {
+                                                   int nqb, int items, int per_xcd) {
   using S = AttnShape<D>;
   constexpr int DK = S::DK, KC = S::KC, DC8 = S::DC8, TV = S::TV, BKV = S::BKV;
   constexpr int KI = S::KI, VI = S::VI;
   __shared__ uint4 sK0[KI * 256], sK1[KI * 256], sK2[KI * 256];
   __shared__ uint4 sV0[VI * 256], sV1[VI * 256], sV2[VI * 256];
 
-  const int head = blockIdx.y;
+  // Work item w = head * nqb + query block.  Workgroups are dealt to the XCDs
+  // round-robin, so workgroup b runs item (b % 8) * per_xcd + b / 8: each XCD
+  // sweeps a contiguous range of items, i.e. the query blocks of one head at a
+  // time, and that head's K and V stay in its L2.
+  const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (w >= items) return;
+  const int head = w / nqb;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
-  const int q0 = blockIdx.x * 128 + wave * 32;
+  const int q0 = (w - head * nqb) * 128 + wave * 32;
   const int ldq = 2 * d;
   const uint16_t* Qb = qk + head * D;
   const uint16_t* Kb = qk + d + head * D;
@@ -93,6 +119,9 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     if (q < M && col < D) v = *reinterpret_cast<const uint4*>(Qb + size_t(q) * ldq + col);
     qf[kk] = __builtin_bit_cast(bf16x8, v);
   }
+  // the query fragments have landed before the first LDS-DMA is issued, so no
+  // later wait on them can also hold up the tile pipeline
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 
   // per-lane source offsets of this wave's DMA instructions for tile 0; tile t
   // adds a uniform t * 64 rows (K) or t * 64 columns (V^T).  K rows run up to
@@ -117,13 +146,9 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     const uint16_t* kt = Kb + size_t(t) * BKV * ldq;
     const uint16_t* vtt = Vb + t * BKV;
 #pragma unroll
-    for (int i = 0; i < KI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(kt + offK[i]),
-                                       (lds_void*)(sk + (wave * KI + i) * 64), 16, 0, 0);
+    for (int i = 0; i < KI; ++i) dma16(kt + offK[i], sk + (wave * KI + i) * 64);
 #pragma unroll
-    for (int i = 0; i < VI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(vtt + offV[i]),
-                                       (lds_void*)(sv + (wave * VI + i) * 64), 16, 0, 0);
+    for (int i = 0; i < VI; ++i) dma16(vtt + offV[i], sv + (wave * VI + i) * 64);
   };
 
   f32x16 o[TV];
@@ -131,7 +156,16 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   for (int t = 0; t < TV; ++t)
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[t][i] = 0.f;
-  float mrow = -INFINITY, lsum = 0.f;
+  // Scores arrive in log2 units (Q pre-scaled by log2(e)/sqrt(d_h)).  One extra
+  // rank-1 MFMA step (k = 8) adds -m to every score: A is a column of ones (the
+  // first k slot of the lanes with g = 0), B holds -m of the lane's query in its
+  // first k slot.  m is kept exactly representable in bf16.
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  const s16x4 kaug = {short(g == 0 ? 0x3F80 : 0), 0, 0, 0};
+  s16x4 qaug = {0, 0, 0, 0};
+  float mrow = 0.f, lsum = 0.f;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
   auto compute = [&](const uint4* sk, const uint4* sv, int t) {
     // S^T for two 32-token sub-tiles; sub-tile st, register i holds token
@@ -139,8 +173,10 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     f32x16 s[2];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
+      f32x16 z;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s[st][i] = 0.f;
+      for (int i = 0; i < 16; ++i) z[i] = 0.f;
+      s[st] = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(kaug, qaug, z, 0, 0, 0);
       const int row = 32 * st + perm_kv(r32);
 #pragma unroll
       for (int kk = 0; kk < DK / 16; ++kk) {
@@ -164,36 +200,33 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
-    // Lazy rescale: keep the running max unless some row of the wave grows by
-    // more than kSlack (log2 units); stale maxima only scale P and the row sum
-    // by at most 2^kSlack, which fp32 accumulation absorbs.
-    if (__builtin_amdgcn_ballot_w64(mx > mrow + kSlack) != 0) {
-      const float mnew = fmaxf(mrow, mx);
-      const float alpha = __builtin_amdgcn_exp2f(mrow - mnew);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));      // tile max of s - m
+    if (t == 0 || __builtin_amdgcn_ballot_w64(mx > kSlack) != 0) {
+      const float mnew = __uint_as_float(uint32_t(to_bf16(mrow + ((t == 0) ? mx : fmaxf(mx, 0.f)))) << 16);
+      const float up = mnew - mrow;                   // exact: both are bf16 values
+      const float alpha = __builtin_amdgcn_exp2f(-up);
       mrow = mnew;
+      qaug[0] = short(to_bf16(-mnew));
       lsum *= alpha;
 #pragma unroll
       for (int tv = 0; tv < TV; ++tv)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[tv][i] *= alpha;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[st][i] -= up;
     }
-    float ps = 0.f;
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float pv = __builtin_amdgcn_exp2f(s[st][i] * scale_log2 - mrow);
-        s[st][i] = pv;
-        ps += pv;
-      }
-    lsum += ps;
     // O^T += V^T P^T over the four 16-token slices of the tile
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       bf16x8 pf;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = static_cast<__bf16>(s[c >> 1][8 * (c & 1) + e]);
+      for (int e = 0; e < 8; ++e) pf[e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[c >> 1][8 * (c & 1) + e]));
+      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 0, 1), one2, lsum, false);
+      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 2, 3), one2, lsum, false);
+      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 4, 5), one2, lsum, false);
+      lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 6, 7), one2, lsum, false);
       const int ch = 2 * c + g;
 #pragma unroll
       for (int tv = 0; tv < TV; ++tv) {
@@ -308,12 +341,14 @@ Status attention_bf16(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t*
     hipLaunchKernelGGL(k_zero_vt_tail, dim3(64), dim3(256), 0, s, v, g.d, ldv, M);
     DC_HIP(hipGetLastError());
   }
-  const float scale_log2 = float(1.4426950408889634 / std::sqrt(double(g.Dh)));
-  dim3 grid((M + 127) / 128, g.H);
+  const int nqb = (M + 127) / 128, items = nqb * g.H, per_xcd = (items + 7) / 8;
+  const dim3 grid(8 * per_xcd);
   if (g.Dh == 64)
-    hipLaunchKernelGGL(k_attn_bf16<64>, grid, dim3(256), 0, s, qk, vt, ldv, out, M, g.d, scale_log2);
+    hipLaunchKernelGGL(k_attn_bf16<64>, grid, dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb, items,
+                       per_xcd);
   else if (g.Dh == 72)
-    hipLaunchKernelGGL(k_attn_bf16<72>, grid, dim3(256), 0, s, qk, vt, ldv, out, M, g.d, scale_log2);
+    hipLaunchKernelGGL(k_attn_bf16<72>, grid, dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb, items,
+                       per_xcd);
   else
     return Status::shape("bf16 attention supports head_dim 64 and 72");
   DC_HIP(hipGetLastError());

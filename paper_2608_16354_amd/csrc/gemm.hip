@@ -8,6 +8,8 @@
 // fp32 GEMMs (patch embedding, timestep MLP).
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
 #include "internal.h"
 
 namespace dc {
@@ -39,11 +41,48 @@ __device__ inline float silu(float z) { return z / (1.0f + expf(-z)); }
 // ---------------------------------------------------------------------------
 // epilogues: operator()(m, n, acc) for one output element
 // ---------------------------------------------------------------------------
+// The MFMA GEMM hands its epilogue one accumulator column at a time: col(mb, n,
+// M, v) gets v[i] = C[mb + 8 (i / 4) + i % 4][n] for i < 16 (mb a multiple of 4),
+// so an epilogue can issue all of its loads for the column before any store.
+// Q (columns < d) leaves pre-multiplied by qscale = log2(e)/sqrt(d_h): the bf16
+// attention kernel takes its scores in log2 units.
 struct EpiQKVBf16 {
-  const float* bias; uint16_t* qk; uint16_t* vt; int d; int ldv;
+  const float* bias; uint16_t* qk; uint16_t* vt; int d; int ldv; float qscale;
+  __device__ void col(int mb, int n, int M, const f32x16& v) const {
+    const float b = bias[n];
+    if (n < d) {
+      uint16_t* __restrict__ q = qk + size_t(mb) * 2 * d + n;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (mb + 8 * (i >> 2) + (i & 3) < M)
+          q[size_t(8 * (i >> 2) + (i & 3)) * 2 * d] = to_bf16((v[i] + b) * qscale);
+    } else if (n < 2 * d) {
+      uint16_t* __restrict__ q = qk + size_t(mb) * 2 * d + n;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (mb + 8 * (i >> 2) + (i & 3) < M) q[size_t(8 * (i >> 2) + (i & 3)) * 2 * d] = to_bf16(v[i] + b);
+    } else {
+      // V^T row n - 2d: four consecutive tokens per 8-byte store (ldv and mb are multiples of 4)
+      uint16_t* __restrict__ r = vt + size_t(n - 2 * d) * ldv + mb;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint2 pk;
+        pk.x = uint32_t(to_bf16(v[4 * g] + b)) | (uint32_t(to_bf16(v[4 * g + 1] + b)) << 16);
+        pk.y = uint32_t(to_bf16(v[4 * g + 2] + b)) | (uint32_t(to_bf16(v[4 * g + 3] + b)) << 16);
+        if (mb + 8 * g + 3 < M) {
+          *reinterpret_cast<uint2*>(r + 8 * g) = pk;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (mb + 8 * g + j < M) r[8 * g + j] = to_bf16(v[4 * g + j] + b);
+        }
+      }
+    }
+  }
   __device__ void operator()(int m, int n, float v) const {
     v += bias[n];
-    if (n < 2 * d) qk[size_t(m) * 2 * d + n] = to_bf16(v);
+    if (n < d) qk[size_t(m) * 2 * d + n] = to_bf16(v * qscale);
+    else if (n < 2 * d) qk[size_t(m) * 2 * d + n] = to_bf16(v);
     else vt[size_t(n - 2 * d) * ldv + m] = to_bf16(v);
   }
 };
@@ -57,6 +96,17 @@ struct EpiQKVF32 {
 };
 struct EpiGateResidual {
   const float* bias; const float* gate; float* h; int ldh;
+  __device__ void col(int mb, int n, int M, const f32x16& v) const {
+    const float g = gate[n], b = bias[n];
+    float* __restrict__ p = h + size_t(mb) * ldh + n;
+    float old[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      old[i] = mb + 8 * (i >> 2) + (i & 3) < M ? p[size_t(8 * (i >> 2) + (i & 3)) * ldh] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (mb + 8 * (i >> 2) + (i & 3) < M) p[size_t(8 * (i >> 2) + (i & 3)) * ldh] = old[i] + g * (v[i] + b);
+  }
   __device__ void operator()(int m, int n, float v) const {
     float* p = h + size_t(m) * ldh + n;
     *p = *p + gate[n] * (v + bias[n]);
@@ -64,6 +114,13 @@ struct EpiGateResidual {
 };
 struct EpiGeluBf16 {
   const float* bias; uint16_t* out; int ldo;
+  __device__ void col(int mb, int n, int M, const f32x16& v) const {
+    const float b = bias[n];
+    uint16_t* __restrict__ o = out + size_t(mb) * ldo + n;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (mb + 8 * (i >> 2) + (i & 3) < M) o[size_t(8 * (i >> 2) + (i & 3)) * ldo] = to_bf16(gelu_tanh(v[i] + b));
+  }
   __device__ void operator()(int m, int n, float v) const {
     out[size_t(m) * ldo + n] = to_bf16(gelu_tanh(v + bias[n]));
   }
@@ -217,7 +274,7 @@ __global__ void __launch_bounds__(256) k_gemm_bf16(const uint16_t* __restrict__ 
 typedef __attribute__((address_space(3))) void lds_void;
 
 template <int BM, int BN, int WM, int WN, class Epi>
-__global__ void __launch_bounds__(512) k_gemm_dma(const uint16_t* __restrict__ A, int lda,
+__global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __restrict__ A, int lda,
                                                   const uint16_t* __restrict__ W, int ldw, int M,
                                                   int N, int K, int tiles_n, int tiles, int per_xcd,
                                                   Epi epi) {
@@ -226,7 +283,7 @@ __global__ void __launch_bounds__(512) k_gemm_dma(const uint16_t* __restrict__ A
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int AI = BM * 8 / 64 / NW, BI = BN * 8 / 64 / NW;   // DMA instructions per wave
-  static_assert(NW == 8 && TM >= 1 && TN >= 1 && AI * NW * 64 == BM * 8 && BI * NW * 64 == BN * 8,
+  static_assert(TM >= 1 && TN >= 1 && AI * NW * 64 == BM * 8 && BI * NW * 64 == BN * 8,
                 "tile shape");
   __shared__ uint4 sA0[BM * 8], sA1[BM * 8];
   __shared__ uint4 sB0[BN * 8], sB1[BN * 8];
@@ -238,18 +295,18 @@ __global__ void __launch_bounds__(512) k_gemm_dma(const uint16_t* __restrict__ A
   const int wm = wave % WM, wn = wave / WM;
 
   // per-lane global element offsets of this wave's DMA instructions (k-step 0)
-  size_t offA[AI], offB[BI];
+  int offA[AI], offB[BI];            // element offsets (operands stay below 2^31 elements)
 #pragma unroll
   for (int i = 0; i < AI; ++i) {
     const int slot = (wave * AI + i) * 64 + lane;
     const int r = slot >> 3, c = (slot & 7) ^ swz(slot >> 3);
-    offA[i] = size_t(min(m0 + r, M - 1)) * lda + 8 * c;
+    offA[i] = min(m0 + r, M - 1) * lda + 8 * c;
   }
 #pragma unroll
   for (int i = 0; i < BI; ++i) {
     const int slot = (wave * BI + i) * 64 + lane;
     const int r = slot >> 3, c = (slot & 7) ^ swz(slot >> 3);
-    offB[i] = size_t(min(n0 + r, N - 1)) * ldw + 8 * c;
+    offB[i] = min(n0 + r, N - 1) * ldw + 8 * c;
   }
   auto issue = [&](uint4* sa, uint4* sb, int kt) {
     const int k0 = kt * BK;
@@ -311,15 +368,13 @@ __global__ void __launch_bounds__(512) k_gemm_dma(const uint16_t* __restrict__ A
   }
 
 #pragma unroll
-  for (int a = 0; a < TM; ++a)
+  for (int b = 0; b < TN; ++b) {
+    const int n = n0 + wn * WTN + b * 32 + r32;
+    if (n < N) {
 #pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int m = m0 + wm * WTM + a * 32 + 8 * (i >> 2) + 4 * hi + (i & 3);
-        const int n = n0 + wn * WTN + b * 32 + r32;
-        if (m < M && n < N) epi(m, n, acc[a][b][i]);
-      }
+      for (int a = 0; a < TM; ++a) epi.col(m0 + wm * WTM + a * 32 + 4 * hi, n, M, acc[a][b]);
+    }
+  }
 }
 
 template <int BM, int BN, int WM, int WN, class Epi>
@@ -327,10 +382,12 @@ Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M,
                   const Epi& epi, hipStream_t s) {
   if (M <= 0) return Status::ok();
   if (K % 64 || lda % 8 || ldw % 8) return Status::shape("bf16 GEMM needs K % 64 == 0 and 16-byte rows");
+  if (int64_t(M) * lda > INT32_MAX || int64_t(N) * ldw > INT32_MAX)
+    return Status::shape("bf16 GEMM operand exceeds 2^31 elements");
   const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
   const int tiles = tn * tm;
   const int per = (tiles + 7) / 8;
-  hipLaunchKernelGGL((k_gemm_dma<BM, BN, WM, WN, Epi>), dim3(8 * per), dim3(512), 0, s, A, lda, W,
+  hipLaunchKernelGGL((k_gemm_dma<BM, BN, WM, WN, Epi>), dim3(8 * per), dim3(WM * WN * 64), 0, s, A, lda, W,
                      ldw, M, N, K, tn, tiles, per, epi);
   DC_HIP(hipGetLastError());
   return Status::ok();
@@ -446,7 +503,9 @@ Status gemm_f32_qkv(const float* A, const float* W, const float* bias, float* qk
 Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, uint16_t* qk,
                      uint16_t* vt, int ldv, const Geo& g, int M, hipStream_t s) {
   return launch_dma<256, 192, 4, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
-                                    EpiQKVBf16{bias, qk, vt, g.d, ldv}, s);
+                                    EpiQKVBf16{bias, qk, vt, g.d, ldv,
+                                               float(1.4426950408889634 / std::sqrt(double(g.Dh)))},
+                                    s);
 }
 
 Status gemm_bf16_gate_residual(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
