@@ -76,7 +76,6 @@ Workspace workspace_layout(const Geo& g, int batch) {
   w.patch = take(size_t(g.Nv) * 64 * 4);
   (void)batch;
   w.drift_part = take(size_t(DC_MAX_BATCH) * kDriftBlocks * 4 * sizeof(double));
-  w.drift_cnt = take(size_t(DC_MAX_BATCH) * sizeof(int32_t));
   w.tm_e = take(size_t(w.kTmax) * 256 * 4);
   w.tm_h = take(size_t(w.kTmax) * g.d * 4);
   w.tm_c = take(size_t(w.kTmax) * g.d * 4);
@@ -146,8 +145,13 @@ Status patch_embed(const Geo& g, const dc_model_weights* w, const float* x, cons
     const int b = il.v[i];
     float* hb = h_in + size_t(b) * g.N * g.d;
     ProfScope ps(KClass::kPatchEmbed, s);
-    DC_TRY(patchify(x + size_t(b) * lat, patches, g, s));
-    DC_TRY(gemm_f32_patch_embed(patches, w->w_pe, w->b_pe, w->pos, g.bf16, hb, g.d, g.Nv, g.d, s));
+    if (g.bf16) {
+      DC_TRY(patch_embed_bf16(x + size_t(b) * lat, w->w_pe, w->b_pe, static_cast<const uint16_t*>(w->pos),
+                              hb, g, s));
+    } else {
+      DC_TRY(patchify(x + size_t(b) * lat, patches, g, s));
+      DC_TRY(gemm_f32_patch_embed(patches, w->w_pe, w->b_pe, w->pos, false, hb, g.d, g.Nv, g.d, s));
+    }
     if (g.Nt > 0) DC_TRY(copy_text(txt + size_t(b) * g.Nt * g.d, hb, g, s));
   }
   return Status::ok();
@@ -239,8 +243,7 @@ Status drift_call(const Geo& g, const float* h_in, const float* mod0, void* u_re
   Workspace L;
   DC_TRY(check_ws(g, std::max(il.n, max_index(il) + 1), ws, ws_bytes, L));
   ProfScope ps(KClass::kDrift, s);
-  return drift(h_in, mod0, u_ref, snapshot != 0, sums, il, g, at<double>(ws, L.drift_part),
-               at<int32_t>(ws, L.drift_cnt), s);
+  return drift(h_in, mod0, u_ref, snapshot != 0, sums, il, g, at<double>(ws, L.drift_part), s);
 }
 
 }  // namespace dc

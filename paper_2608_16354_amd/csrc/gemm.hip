@@ -1,11 +1,14 @@
 // GEMMs of the denoising step: C = A W^T with fused epilogues.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16 tiles (gfx950), 256 threads = 4 waves,
-// block tile BM x BN x 64, double-buffered LDS with an XOR swizzle on the 16-byte
-// chunks of each 128-byte row (conflict-free reads of 16 rows by 16 lanes), one barrier per k-step, the next k-tile prefetched into
-// registers while the current one is multiplied.
-// f32 path: a plain SIMT tiled kernel for the fp32 model and the small
-// fp32 GEMMs (patch embedding, timestep MLP).
+// bf16 block GEMMs (QKV, out-projection, MLP up / down): v_mfma_f32_32x32x16_bf16,
+// 8 waves, block tile 256 x 192 x 64, tiles fed global -> LDS by LDS-DMA into two
+// stages, XOR-swizzled 128-byte rows, one barrier per k-step, XCD-aware tile
+// order; epilogues take one accumulator column at a time.
+// bf16 head + Euler: a streaming kernel (A straight from HBM into MFMA
+// registers, the contraction split over the four waves of a workgroup).
+// bf16 patch embedding: fp32-accurate split-bf16 MFMA with the patchify gather fused.
+// f32 path: a plain SIMT tiled kernel for the fp32 model and the small fp32
+// GEMMs (patch embedding of the fp32 model, timestep MLP).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -50,17 +53,17 @@ struct EpiQKVBf16 {
   const float* bias; uint16_t* qk; uint16_t* vt; int d; int ldv; float qscale;
   __device__ void col(int mb, int n, int M, const f32x16& v) const {
     const float b = bias[n];
-    if (n < d) {
+    if (n < 2 * d) {
+      const float sc = n < d ? qscale : 1.0f;
       uint16_t* __restrict__ q = qk + size_t(mb) * 2 * d + n;
+      if (mb + 28 <= M) {                     // all 16 rows present: no per-row guards
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (mb + 8 * (i >> 2) + (i & 3) < M)
-          q[size_t(8 * (i >> 2) + (i & 3)) * 2 * d] = to_bf16((v[i] + b) * qscale);
-    } else if (n < 2 * d) {
-      uint16_t* __restrict__ q = qk + size_t(mb) * 2 * d + n;
+        for (int i = 0; i < 16; ++i) q[size_t(8 * (i >> 2) + (i & 3)) * 2 * d] = to_bf16((v[i] + b) * sc);
+      } else {
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (mb + 8 * (i >> 2) + (i & 3) < M) q[size_t(8 * (i >> 2) + (i & 3)) * 2 * d] = to_bf16(v[i] + b);
+        for (int i = 0; i < 16; ++i)
+          if (mb + 8 * (i >> 2) + (i & 3) < M) q[size_t(8 * (i >> 2) + (i & 3)) * 2 * d] = to_bf16((v[i] + b) * sc);
+      }
     } else {
       // V^T row n - 2d: four consecutive tokens per 8-byte store (ldv and mb are multiples of 4)
       uint16_t* __restrict__ r = vt + size_t(n - 2 * d) * ldv + mb;
@@ -99,10 +102,20 @@ struct EpiGateResidual {
   __device__ void col(int mb, int n, int M, const f32x16& v) const {
     const float g = gate[n], b = bias[n];
     float* __restrict__ p = h + size_t(mb) * ldh + n;
+    if (mb + 28 <= M) {                       // all 16 rows present: batched loads, no guards
+      float old[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) old[i] = p[size_t(8 * (i >> 2) + (i & 3)) * ldh];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) p[size_t(8 * (i >> 2) + (i & 3)) * ldh] = old[i] + g * (v[i] + b);
+      return;
+    }
     float old[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      old[i] = mb + 8 * (i >> 2) + (i & 3) < M ? p[size_t(8 * (i >> 2) + (i & 3)) * ldh] : 0.f;
+    for (int i = 0; i < 16; ++i) {
+      const int r = min(mb + 8 * (i >> 2) + (i & 3), M - 1) - mb;   // clamped: in bounds
+      old[i] = p[size_t(r) * ldh];
+    }
 #pragma unroll
     for (int i = 0; i < 16; ++i)
       if (mb + 8 * (i >> 2) + (i & 3) < M) p[size_t(8 * (i >> 2) + (i & 3)) * ldh] = old[i] + g * (v[i] + b);
@@ -117,9 +130,14 @@ struct EpiGeluBf16 {
   __device__ void col(int mb, int n, int M, const f32x16& v) const {
     const float b = bias[n];
     uint16_t* __restrict__ o = out + size_t(mb) * ldo + n;
+    if (mb + 28 <= M) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (mb + 8 * (i >> 2) + (i & 3) < M) o[size_t(8 * (i >> 2) + (i & 3)) * ldo] = to_bf16(gelu_tanh(v[i] + b));
+      for (int i = 0; i < 16; ++i) o[size_t(8 * (i >> 2) + (i & 3)) * ldo] = to_bf16(gelu_tanh(v[i] + b));
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (mb + 8 * (i >> 2) + (i & 3) < M) o[size_t(8 * (i >> 2) + (i & 3)) * ldo] = to_bf16(gelu_tanh(v[i] + b));
+    }
   }
   __device__ void operator()(int m, int n, float v) const {
     out[size_t(m) * ldo + n] = to_bf16(gelu_tanh(v + bias[n]));
@@ -149,6 +167,25 @@ struct EpiPatch {
 // Head + Euler: token m, patch-vector index n -> latent element; x += dsigma * (acc + b).
 struct EpiHeadEuler {
   const float* bias; float* x; float dsigma; int T, Hl, Wl, p, Hp, Wp;
+  __device__ float* at(int m, int n) const {
+    const int pp = p * p;
+    const int c = n / pp, a = (n / p) % p, b = n % p;
+    const int t = m / (Hp * Wp), i = (m / Wp) % Hp, j = m % Wp;
+    return x + ((size_t(c) * T + t) * Hl + (p * i + a)) * Wl + (p * j + b);
+  }
+  // rows mb + 8 (i / 4) + i % 4 of output column n: all loads, then all stores
+  __device__ void col(int mb, int n, int M, const float (&v)[16]) const {
+    const float bn = bias[n];
+    float* dst[16];
+    float old[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) dst[i] = at(min(mb + 8 * (i >> 2) + (i & 3), M - 1), n);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) old[i] = *dst[i];
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (mb + 8 * (i >> 2) + (i & 3) < M) *dst[i] = old[i] + dsigma * (v[i] + bn);
+  }
   __device__ void operator()(int m, int n, float v) const {
     const int pp = p * p;
     const int c = n / pp, a = (n / p) % p, b = n % p;
@@ -157,107 +194,6 @@ struct EpiHeadEuler {
     *dst = *dst + dsigma * (v + bias[n]);
   }
 };
-
-// ---------------------------------------------------------------------------
-// bf16 MFMA GEMM
-// ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, class Epi>
-__global__ void __launch_bounds__(256) k_gemm_bf16(const uint16_t* __restrict__ A, int lda,
-                                                   const uint16_t* __restrict__ W, int ldw, int M,
-                                                   int N, int K, Epi epi) {
-  constexpr int BK = 64;
-  constexpr int WTM = BM / WM, WTN = BN / WN;     // wave tile
-  constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA tiles per wave
-  constexpr int AC = BM * 8 / 256, BC = BN * 8 / 256;   // 16-B chunks per thread
-  static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && AC >= 1 && BC >= 1, "tile shape");
-  __shared__ uint4 sA[2][BM * 8];
-  __shared__ uint4 sB[2][BN * 8];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave % WM, wn = wave / WM;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int lc = tid & 7, lr = tid >> 3;          // loader: chunk, base row
-
-  uint4 ra[AC], rb[BC];
-  auto gload = [&](int kt) {
-    const int k0 = kt * BK + lc * 8;
-#pragma unroll
-    for (int i = 0; i < AC; ++i) {
-      const int gm = m0 + lr + 32 * i;
-      ra[i] = gm < M ? *reinterpret_cast<const uint4*>(A + size_t(gm) * lda + k0)
-                     : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < BC; ++i) {
-      const int gn = n0 + lr + 32 * i;
-      rb[i] = *reinterpret_cast<const uint4*>(W + size_t(gn) * ldw + k0);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < AC; ++i) {
-      const int r = lr + 32 * i;
-      sA[buf][r * 8 + (lc ^ swz(r))] = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BC; ++i) {
-      const int r = lr + 32 * i;
-      sB[buf][r * 8 + (lc ^ swz(r))] = rb[i];
-    }
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
-
-  const int KT = K / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int r32 = lane & 31, hi = lane >> 5;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int ch = kk * 2 + hi;
-      bf16x8 af[TM], bf[TN];
-#pragma unroll
-      for (int a = 0; a < TM; ++a) {
-        const int r = wm * WTM + a * 32 + r32;
-        af[a] = __builtin_bit_cast(bf16x8, sA[cur][r * 8 + (ch ^ swz(r))]);
-      }
-#pragma unroll
-      for (int b = 0; b < TN; ++b) {
-        const int r = wn * WTN + b * 32 + r32;
-        bf[b] = __builtin_bit_cast(bf16x8, sB[cur][r * 8 + (ch ^ swz(r))]);
-      }
-#pragma unroll
-      for (int a = 0; a < TM; ++a)
-#pragma unroll
-        for (int b = 0; b < TN; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[b], acc[a][b], 0, 0, 0);
-    }
-    if (kt + 1 < KT) sstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  // 32x32 accumulator layout: lane l, register i -> row 8(i/4) + 4(l/32) + i%4, column l%32.
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int m = m0 + wm * WTM + a * 32 + 8 * (i >> 2) + 4 * hi + (i & 3);
-        const int n = n0 + wn * WTN + b * 32 + r32;
-        if (m < M) epi(m, n, acc[a][b][i]);
-      }
-}
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA GEMM, LDS-DMA pipeline.  512 threads = 8 waves (2 per SIMD), block
@@ -393,16 +329,180 @@ Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M,
   return Status::ok();
 }
 
-template <int BM, int BN, int WM, int WN, class Epi>
-Status launch_bf16(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M, int N, int K,
-                   const Epi& epi, hipStream_t s) {
-  if (M <= 0) return Status::ok();
-  if (N % BN || K % 64) return Status::shape("bf16 GEMM needs N % tile == 0 and K % 64 == 0");
-  dim3 grid(N / BN, (M + BM - 1) / BM);
-  hipLaunchKernelGGL((k_gemm_bf16<BM, BN, WM, WN, Epi>), grid, dim3(256), 0, s, A, lda, W, ldw, M,
-                     N, K, epi);
-  DC_HIP(hipGetLastError());
-  return Status::ok();
+
+// ---------------------------------------------------------------------------
+// Head + Euler (bf16): x += dsigma * (A W^T + b) with A [M, d] bf16 (the
+// modulated final hidden state), W [64, d] bf16, scattered into the latent.
+// N = 64 outputs per token and each A element is used once, so the kernel
+// streams A straight from HBM into MFMA registers (no LDS staging).  A workgroup
+// owns 64 tokens; its four waves split d into quarters and each accumulates a
+// 64 x 64 partial; the partials meet in LDS and are added in wave order
+// (reproducible), each wave finishing one 32 x 32 output tile.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_head_bf16(const uint16_t* __restrict__ A, int lda,
+                                                   const uint16_t* __restrict__ W, int d, int M,
+                                                   EpiHeadEuler epi) {
+  __shared__ float part[4][4][16][64];     // [wave][tile][register][lane]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r32 = lane & 31, hi = lane >> 5;
+  const int m0 = blockIdx.x * 64;
+  const int kq = d >> 2, k0 = wave * kq;   // this wave's quarter of the contraction
+  const uint16_t* arow[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) arow[a] = A + size_t(min(m0 + 32 * a + r32, M - 1)) * lda + k0 + 8 * hi;
+  const uint16_t* wrow[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) wrow[b] = W + size_t(32 * b + r32) * d + k0 + 8 * hi;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
+  // groups of four 16-wide slices (kq is a multiple of 32), double-buffered:
+  // the loads of group g + 1 are in flight while group g is multiplied
+  bf16x8 af[2][4][2], bf[2][4][2];
+  auto load = [&](int buf, int k) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (k + 16 * j < kq) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a) af[buf][j][a] = *reinterpret_cast<const bf16x8*>(arow[a] + k + 16 * j);
+#pragma unroll
+        for (int b = 0; b < 2; ++b) bf[buf][j][b] = *reinterpret_cast<const bf16x8*>(wrow[b] + k + 16 * j);
+      }
+  };
+  auto mma = [&](int buf, int k) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (k + 16 * j < kq) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[buf][j][a], bf[buf][j][b], acc[a][b], 0, 0, 0);
+      }
+  };
+  load(0, 0);
+  for (int k = 0; k < kq; k += 128) {
+    if (k + 64 < kq) load(1, k + 64);
+    mma(0, k);
+    if (k + 64 >= kq) break;
+    if (k + 128 < kq) load(0, k + 128);
+    mma(1, k + 64);
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) part[wave][t][i][lane] = acc[t >> 1][t & 1][i];
+  __syncthreads();
+  // wave w finishes output tile w: token rows 32 (w / 2) + ..., outputs 32 (w % 2) + r32
+  const int n = 32 * (wave & 1) + r32;
+  const int mb = m0 + 32 * (wave >> 1) + 4 * hi;
+  float v[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    v[i] = ((part[0][wave][i][lane] + part[1][wave][i][lane]) + part[2][wave][i][lane]) +
+           part[3][wave][i][lane];
+  epi.col(mb, n, M, v);
+}
+
+// ---------------------------------------------------------------------------
+// Patch embedding for the bf16 model: h_in[n] = patch(x)[n] W_pe^T + b + pos[n]
+// with the fp32 latent and fp32 W_pe kept at fp32 accuracy on bf16 MFMA: each
+// operand is split v = hi + lo (hi = bf16(v), lo = bf16(v - hi)) and the
+// product is hi*Whi + lo*Whi + hi*Wlo (the dropped lo*Wlo is ~2^-18 relative).
+// The patchify gather is fused: each lane reads its 8 patch-vector entries
+// straight from the latent.  A workgroup = 8 waves x 32 tokens x a 128-wide
+// column chunk; the chunk of W_pe is split once into LDS and shared.
+// ---------------------------------------------------------------------------
+struct PatchGeo { int T, Hl, Wl, p, lp, Hp, Wp; };   // lp = log2(p)
+
+__global__ void __launch_bounds__(512) k_patch_embed_bf16(const float* __restrict__ x,
+                                                          const float* __restrict__ W,
+                                                          const float* __restrict__ bias,
+                                                          const uint16_t* __restrict__ pos,
+                                                          float* __restrict__ out, int Nv, int d,
+                                                          PatchGeo pg) {
+  __shared__ uint4 wh[128 * 8], wl[128 * 8];     // [n][16-byte chunk of k], swizzled
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r32 = lane & 31, hi = lane >> 5;
+  const int n0 = blockIdx.y * 128;
+  // stage W[n0 .. n0 + 128)[0 .. 64) as bf16 hi / lo: thread -> (row, 4 chunks of 4 k)
+  {
+    const int n = tid >> 2, k4 = (tid & 3) * 16;    // 16 consecutive k per thread
+    const float4* src = reinterpret_cast<const float4*>(W + size_t(n0 + n) * 64 + k4);
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = src[q];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float f[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+      uint16_t h[4], l[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        h[j] = to_bf16(f[j]);
+        l[j] = to_bf16(f[j] - from_bf16(h[j]));
+      }
+      const int k = k4 + 4 * q;
+      const int e = n * 64 + ((k >> 3) ^ swz(n)) * 8 + (k & 7);   // bf16 index, 8-byte aligned
+      *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(wh) + e) =
+          make_uint2(h[0] | (uint32_t(h[1]) << 16), h[2] | (uint32_t(h[3]) << 16));
+      *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(wl) + e) =
+          make_uint2(l[0] | (uint32_t(l[1]) << 16), l[2] | (uint32_t(l[3]) << 16));
+    }
+  }
+  // A fragments: token m, patch-vector entries 16 kk + 8 hi + e
+  const int m0 = blockIdx.x * 256 + wave * 32;
+  const int m = min(m0 + r32, Nv - 1);
+  const int t = m / (pg.Hp * pg.Wp), i = (m / pg.Wp) % pg.Hp, j = m % pg.Wp;
+  bf16x8 ah[4], al[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int q = 16 * kk + 8 * hi + e;
+      const int c = q >> (2 * pg.lp), a = (q >> pg.lp) & (pg.p - 1), b = q & (pg.p - 1);
+      const float v = x[((size_t(c) * pg.T + t) * pg.Hl + (pg.p * i + a)) * pg.Wl + (pg.p * j + b)];
+      const __bf16 h = static_cast<__bf16>(v);
+      ah[kk][e] = h;
+      al[kk][e] = static_cast<__bf16>(v - static_cast<float>(h));
+    }
+  __syncthreads();
+#pragma unroll
+  for (int tile = 0; tile < 4; ++tile) {
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    const int nr = 32 * tile + r32;                 // row of the LDS chunk
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int ch = (2 * kk + hi) ^ swz(nr);
+      const bf16x8 bh = __builtin_bit_cast(bf16x8, wh[nr * 8 + ch]);
+      const bf16x8 bl = __builtin_bit_cast(bf16x8, wl[nr * 8 + ch]);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[kk], bh, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[kk], bh, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[kk], bl, acc, 0, 0, 0);
+    }
+    const int n = n0 + nr;
+    const float bn = bias[n];
+    float pv[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)   // rows clamped into the table: all 16 loads issue together
+      pv[r] = from_bf16(pos[size_t(min(m0 + 8 * (r >> 2) + 4 * hi + (r & 3), Nv - 1)) * d + n]);
+    if (m0 + 32 <= Nv) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        out[size_t(m0 + 8 * (r >> 2) + 4 * hi + (r & 3)) * d + n] = (acc[r] + bn) + pv[r];
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int mm = m0 + 8 * (r >> 2) + 4 * hi + (r & 3);
+        if (mm < Nv) out[size_t(mm) * d + n] = (acc[r] + bn) + pv[r];
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -521,8 +621,26 @@ Status gemm_bf16_gelu(const uint16_t* A, int lda, const uint16_t* W, const float
 
 Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float* bias, float* x,
                       float dsigma, const Geo& g, int M, hipStream_t s) {
+  if (M <= 0) return Status::ok();
+  if (g.P != 64 || g.d % 128 || lda % 8) return Status::shape("bf16 head needs 64 outputs and d % 128 == 0");
   EpiHeadEuler e{bias, x, dsigma, g.T, g.Hl, g.Wl, g.p, g.Hp, g.Wp};
-  return launch_bf16<64, 64, 2, 2>(A, lda, W, g.d, M, g.P, g.d, e, s);
+  hipLaunchKernelGGL(k_head_bf16, dim3((M + 63) / 64), dim3(256), 0, s, A, lda, W, g.d, M, e);
+  DC_HIP(hipGetLastError());
+  return Status::ok();
+}
+
+Status patch_embed_bf16(const float* x, const float* W, const float* bias, const uint16_t* pos,
+                        float* out, const Geo& g, hipStream_t s) {
+  if (g.Nv <= 0) return Status::ok();
+  if (g.P != 64 || g.d % 128) return Status::shape("bf16 patch embedding needs 64-entry patches, d % 128 == 0");
+  int lp = 0;
+  while ((1 << lp) < g.p) ++lp;
+  if ((1 << lp) != g.p) return Status::shape("bf16 patch embedding needs a power-of-two patch");
+  const PatchGeo pg{g.T, g.Hl, g.Wl, g.p, lp, g.Hp, g.Wp};
+  hipLaunchKernelGGL(k_patch_embed_bf16, dim3((g.Nv + 255) / 256, g.d / 128), dim3(512), 0, s, x, W,
+                     bias, pos, out, g.Nv, g.d, pg);
+  DC_HIP(hipGetLastError());
+  return Status::ok();
 }
 
 }  // namespace dc

@@ -92,13 +92,13 @@ Status make_idx(const int32_t* idx, int32_t n, IdxList& out);
 
 // Workspace layout (offsets in bytes, each 256-aligned).
 struct Workspace {
-  size_t a, qk, vt, o, ff, patch, drift_part, drift_cnt, tm_e, tm_h, tm_c, tm_s, tm_m, total;
+  size_t a, qk, vt, o, ff, patch, drift_part, tm_e, tm_h, tm_c, tm_s, tm_m, total;
   int ldv;               // row stride of the transposed value buffer (tokens, padded)
   int kTmax;             // steps the modulation scratch can hold per pass
 };
 Workspace workspace_layout(const Geo& g, int batch);
 
-constexpr int kDriftBlocks = 512;   // fixed grid per sample: reproducible reductions
+constexpr int kDriftBlocks = 1024;  // fixed grid per sample: reproducible reductions
 
 // ---------------------------------------------------------------------------
 // kernel launchers (kernels_*.hip, gemm.hip, attention.hip)
@@ -128,6 +128,9 @@ Status gemm_bf16_gate_residual(const uint16_t* A, int lda, const uint16_t* W, co
                                hipStream_t s);
 Status gemm_bf16_gelu(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
                       uint16_t* out, int ldo, int M, int N, int K, hipStream_t s);
+// bf16 model: fused patchify + patch embedding (+ bias + positional table) for one sample.
+Status patch_embed_bf16(const float* x, const float* W, const float* bias, const uint16_t* pos,
+                        float* out, const Geo& g, hipStream_t s);
 Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float* bias, float* x,
                       float dsigma, const Geo& g, int M, hipStream_t s);
 
@@ -145,7 +148,7 @@ Status cache_store(const float* h_out, const float* h_in, void* resid, const Idx
 Status cache_apply(const float* h_in, const void* resid, float* gout, const IdxList& idx,
                    const Geo& g, hipStream_t s);
 Status drift(const float* h_in, const float* mod0, void* u_ref, bool snapshot, double* sums,
-             const IdxList& idx, const Geo& g, double* part, int32_t* cnt, hipStream_t s);
+             const IdxList& idx, const Geo& g, double* part, hipStream_t s);
 Status patchify(const float* x, float* patches, const Geo& g, hipStream_t s);
 Status copy_text(const float* txt, float* h_in, const Geo& g, hipStream_t s);
 Status copy_rows(const float* src, float* dst, size_t count, hipStream_t s);

@@ -4,6 +4,8 @@
 // vector accesses.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace dc {
@@ -11,7 +13,6 @@ namespace dc {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kMaxVec = 12;   // float4 per lane per row: rows up to 64 * 12 * 4 = 3072 wide
 
 __device__ inline float wave_sum(float v) {
 #pragma unroll
@@ -25,38 +26,31 @@ __device__ inline uint16_t to_bf16(float f) {
 }
 __device__ inline float from_bf16(uint16_t u) { return __uint_as_float(uint32_t(u) << 16); }
 
-// Load one row of `d` floats (d % 4 == 0) into registers, lane-strided float4.
-__device__ inline int load_row(const float* __restrict__ row, int d, int lane, float4 (&v)[kMaxVec]) {
-  const int n4 = d >> 2;
-  int cnt = 0;
+// Branch-free row load for rows of n4 float4 with NV = ceil(n4 / 64) per lane: lanes
+// past the row re-read its last float4 (in bounds) and are masked in the sums, so
+// all NV loads issue back to back.
+template <int NV>
+__device__ inline void load_row_nv(const float* __restrict__ row, int n4, int lane, float4 (&v)[NV]) {
+  const float4* r4 = reinterpret_cast<const float4*>(row);
 #pragma unroll
-  for (int i = 0; i < kMaxVec; ++i) {
-    const int c = lane + i * kWave;
-    if (c < n4) {
-      v[i] = reinterpret_cast<const float4*>(row)[c];
-      cnt = i + 1;
-    }
-  }
-  return cnt;
+  for (int i = 0; i < NV; ++i) v[i] = r4[min(lane + i * kWave, n4 - 1)];
 }
 
-// Mean and reciprocal standard deviation of a register-resident row (two passes).
-__device__ inline void row_stats(const float4 (&v)[kMaxVec], int d, int lane, float eps,
-                                 float& mean, float& rstd) {
-  const int n4 = d >> 2;
+template <int NV>
+__device__ inline void row_stats_nv(const float4 (&v)[NV], int n4, int lane, float eps, float& mean,
+                                    float& rstd) {
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxVec; ++i)
-    if (lane + i * kWave < n4) s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
-  mean = wave_sum(s) / float(d);
+  for (int i = 0; i < NV; ++i)
+    s += (lane + i * kWave < n4) ? (v[i].x + v[i].y) + (v[i].z + v[i].w) : 0.f;
+  mean = wave_sum(s) / float(4 * n4);
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxVec; ++i)
-    if (lane + i * kWave < n4) {
-      const float a = v[i].x - mean, b = v[i].y - mean, c = v[i].z - mean, e = v[i].w - mean;
-      q += (a * a + b * b) + (c * c + e * e);
-    }
-  const float var = wave_sum(q) / float(d);
+  for (int i = 0; i < NV; ++i) {
+    const float a = v[i].x - mean, b = v[i].y - mean, c = v[i].z - mean, e = v[i].w - mean;
+    q += (lane + i * kWave < n4) ? (a * a + b * b) + (c * c + e * e) : 0.f;
+  }
+  const float var = wave_sum(q) / float(4 * n4);
   rstd = 1.0f / sqrtf(var + eps);
 }
 
@@ -87,7 +81,8 @@ __device__ inline float4 load4(const void* in, size_t e, bool bf) {
   return *reinterpret_cast<const float4*>(static_cast<const float*>(in) + e);
 }
 
-// a = LN(x)(1 + scale) + shift, one wavefront per row.
+// a = LN(x)(1 + scale) + shift, one wavefront per row (NV float4 per lane).
+template <int NV>
 __global__ void __launch_bounds__(256) k_ln_modulate(const float* __restrict__ x, int rows, int ldx,
                                                      const float* __restrict__ shift,
                                                      const float* __restrict__ scale, void* out,
@@ -95,19 +90,18 @@ __global__ void __launch_bounds__(256) k_ln_modulate(const float* __restrict__ x
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
-  float4 v[kMaxVec];
-  load_row(x + size_t(row) * ldx, d, lane, v);
-  float mean, rstd;
-  row_stats(v, d, lane, eps, mean, rstd);
   const int n4 = d >> 2;
+  float4 v[NV];
+  load_row_nv<NV>(x + size_t(row) * ldx, n4, lane, v);
+  float mean, rstd;
+  row_stats_nv<NV>(v, n4, lane, eps, mean, rstd);
 #pragma unroll
-  for (int i = 0; i < kMaxVec; ++i) {
-    const int c = lane + i * kWave;
-    if (c < n4) {
-      const float4 sh = reinterpret_cast<const float4*>(shift)[c];
-      const float4 sc = reinterpret_cast<const float4*>(scale)[c];
-      store4(out, size_t(row) * ldo + 4 * c, modulate4(v[i], mean, rstd, sh, sc), bf);
-    }
+  for (int i = 0; i < NV; ++i) {
+    const int c = min(lane + i * kWave, n4 - 1);
+    const float4 sh = reinterpret_cast<const float4*>(shift)[c];
+    const float4 sc = reinterpret_cast<const float4*>(scale)[c];
+    const float4 u = modulate4(v[i], mean, rstd, sh, sc);
+    if (lane + i * kWave < n4) store4(out, size_t(row) * ldo + 4 * c, u, bf);
   }
 }
 
@@ -144,16 +138,20 @@ __global__ void __launch_bounds__(256) k_cache_apply(const float* __restrict__ h
 }
 
 // Drift: u = LN(h_in[:N_v])(1+scale)+shift; either snapshot u into u_ref, or
-// accumulate (sum|u-u_ref|, sum|u|, sum(u-u_ref)^2, sum u^2).  Per-lane fp32 row
-// partials -> wave shuffle reduction -> per-block f64 partial in a fixed order ->
-// a cross-block atomic ticket elects the last block, which adds the block
-// partials in index order.  The result is bitwise reproducible.
+// accumulate (sum|u-u_ref|, sum|u|, sum(u-u_ref)^2, sum u^2).  One wavefront per
+// row; the row of u_ref is fetched together with the row of h_in (it does not
+// depend on the row statistics), so each row costs one memory round trip.
+// Per-lane fp32 row partials -> wave shuffle reduction -> per-block f64 partial
+// in a fixed order; k_drift_reduce adds the block partials in a fixed order.
+// For a given N_v the result is bitwise reproducible.
+template <bool BF, int NV>
 __global__ void __launch_bounds__(256) k_drift(const float* __restrict__ h_in,
                                                const float* __restrict__ mod0, void* u_ref,
-                                               int snapshot, double* __restrict__ sums,
-                                               IdxList idx, int Nv, int d, size_t stride_h,
-                                               size_t stride_r, float eps, bool bf,
-                                               double* __restrict__ part, int32_t* cnt) {
+                                               int snapshot, IdxList idx, int Nv, int d,
+                                               size_t stride_h,
+                                               size_t stride_r, float eps,
+                                               double* __restrict__ part) {
+  typedef typename std::conditional<BF, uint2, float4>::type RV;   // 4 elements of u_ref
   const int b = idx.v[blockIdx.y];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float* shift = mod0;
@@ -163,29 +161,41 @@ __global__ void __launch_bounds__(256) k_drift(const float* __restrict__ h_in,
   const int n4 = d >> 2;
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
   for (int row = blockIdx.x * 4 + wave; row < Nv; row += gridDim.x * 4) {
-    float4 v[kMaxVec];
-    load_row(hb + size_t(row) * d, d, lane, v);
+    float4 v[NV];
+    RV r[NV];
+    load_row_nv<NV>(hb + size_t(row) * d, n4, lane, v);
+    const RV* rrow = reinterpret_cast<const RV*>(static_cast<const char*>(u_ref) +
+                                                 (rbase + size_t(row) * d) * (BF ? 2 : 4));
+    if (!snapshot) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) r[i] = rrow[min(lane + i * kWave, n4 - 1)];
+    }
     float mean, rstd;
-    row_stats(v, d, lane, eps, mean, rstd);
+    row_stats_nv<NV>(v, n4, lane, eps, mean, rstd);
     float s1 = 0.f, s2 = 0.f, s3 = 0.f, s4 = 0.f;
 #pragma unroll
-    for (int i = 0; i < kMaxVec; ++i) {
-      const int c = lane + i * kWave;
-      if (c < n4) {
-        const float4 sh = reinterpret_cast<const float4*>(shift)[c];
-        const float4 sc = reinterpret_cast<const float4*>(scale)[c];
-        const float4 u = modulate4(v[i], mean, rstd, sh, sc);
-        const size_t e = rbase + size_t(row) * d + 4 * c;
-        if (snapshot) {
-          store4(u_ref, e, u, bf);
+    for (int i = 0; i < NV; ++i) {
+      const bool ok = lane + i * kWave < n4;
+      const int c = min(lane + i * kWave, n4 - 1);
+      const float4 sh = reinterpret_cast<const float4*>(shift)[c];
+      const float4 sc = reinterpret_cast<const float4*>(scale)[c];
+      const float4 u = modulate4(v[i], mean, rstd, sh, sc);
+      if (snapshot) {
+        if (ok) store4(u_ref, rbase + size_t(row) * d + 4 * c, u, BF);
+      } else {
+        float4 q;
+        if constexpr (BF) {
+          const uint2 w = r[i];
+          q = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u),
+                          __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xFFFF0000u));
         } else {
-          const float4 r = load4(u_ref, e, bf);
-          const float dx = u.x - r.x, dy = u.y - r.y, dz = u.z - r.z, dw = u.w - r.w;
-          s1 += (fabsf(dx) + fabsf(dy)) + (fabsf(dz) + fabsf(dw));
-          s2 += (fabsf(u.x) + fabsf(u.y)) + (fabsf(u.z) + fabsf(u.w));
-          s3 += (dx * dx + dy * dy) + (dz * dz + dw * dw);
-          s4 += (u.x * u.x + u.y * u.y) + (u.z * u.z + u.w * u.w);
+          q = r[i];
         }
+        const float dx = u.x - q.x, dy = u.y - q.y, dz = u.z - q.z, dw = u.w - q.w;
+        s1 += ok ? (fabsf(dx) + fabsf(dy)) + (fabsf(dz) + fabsf(dw)) : 0.f;
+        s2 += ok ? (fabsf(u.x) + fabsf(u.y)) + (fabsf(u.z) + fabsf(u.w)) : 0.f;
+        s3 += ok ? (dx * dx + dy * dy) + (dz * dz + dw * dw) : 0.f;
+        s4 += ok ? (u.x * u.x + u.y * u.y) + (u.z * u.z + u.w * u.w) : 0.f;
       }
     }
     if (!snapshot) {
@@ -195,32 +205,33 @@ __global__ void __launch_bounds__(256) k_drift(const float* __restrict__ h_in,
   }
   if (snapshot) return;
   __shared__ double wsum[4][4];
-  __shared__ int last;
   if (lane == 0)
     for (int q = 0; q < 4; ++q) wsum[wave][q] = acc[q];
   __syncthreads();
-  if (threadIdx.x == 0) {
-    double* pb = part + (size_t(blockIdx.y) * gridDim.x + blockIdx.x) * 4;
-    for (int q = 0; q < 4; ++q) pb[q] = ((wsum[0][q] + wsum[1][q]) + wsum[2][q]) + wsum[3][q];
-    __threadfence();
-    const int ticket = atomicAdd(&cnt[blockIdx.y], 1);
-    last = (ticket == int(gridDim.x) - 1);
-  }
-  __syncthreads();
-  if (last && threadIdx.x < 4) {
-    __threadfence();
-    const double* pb = part + size_t(blockIdx.y) * gridDim.x * 4;
-    double s = 0.0;
-    for (unsigned i = 0; i < gridDim.x; ++i)
-      s += __hip_atomic_load(pb + 4 * i + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    sums[size_t(b) * 4 + threadIdx.x] = s;
-    if (threadIdx.x == 0) cnt[blockIdx.y] = 0;
+  if (threadIdx.x < 4) {
+    const int q = threadIdx.x;
+    part[(size_t(blockIdx.y) * gridDim.x + blockIdx.x) * 4 + q] =
+        ((wsum[0][q] + wsum[1][q]) + wsum[2][q]) + wsum[3][q];
   }
 }
 
-__global__ void k_zero_i32(int32_t* p, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0;
+// Second pass of the drift reduction (one workgroup per sample): the nb block
+// partials in a fixed order, 64 strided f64 chains per quantity, then a fixed
+// tree.  The kernel boundary orders it after every partial.
+__global__ void __launch_bounds__(256) k_drift_reduce(const double* __restrict__ part, int nb,
+                                                      IdxList idx, double* __restrict__ sums) {
+  __shared__ double red[64][4];
+  const int q = threadIdx.x & 3, j = threadIdx.x >> 2;
+  const double* pb = part + size_t(blockIdx.x) * nb * 4;
+  double s = 0.0;
+  for (int i = j; i < nb; i += 64) s += pb[4 * i + q];
+  red[j][q] = s;
+  __syncthreads();
+  for (int w = 32; w >= 1; w >>= 1) {
+    if (j < w) red[j][q] += red[j + w][q];
+    __syncthreads();
+  }
+  if (threadIdx.x < 4) sums[size_t(idx.v[blockIdx.x]) * 4 + threadIdx.x] = red[0][threadIdx.x];
 }
 
 // patches[n, c p^2 + a p + b] = x[c, t, p i + a, p j + b], n = (t Hp + i) Wp + j.
@@ -293,11 +304,34 @@ inline int grid_for(size_t n, int per_block, int cap) {
 
 #define DC_LAUNCH_CHECK() DC_HIP(hipGetLastError())
 
+// Calls f(std::integral_constant<int, NV>) with NV = ceil(d / 256) float4 per lane.
+template <class F>
+Status with_nv(int d, F&& f) {
+  switch ((d + 255) / 256) {
+    case 1: f(std::integral_constant<int, 1>{}); break;
+    case 2: f(std::integral_constant<int, 2>{}); break;
+    case 3: f(std::integral_constant<int, 3>{}); break;
+    case 4: f(std::integral_constant<int, 4>{}); break;
+    case 5: f(std::integral_constant<int, 5>{}); break;
+    case 6: f(std::integral_constant<int, 6>{}); break;
+    case 7: f(std::integral_constant<int, 7>{}); break;
+    case 8: f(std::integral_constant<int, 8>{}); break;
+    case 9: f(std::integral_constant<int, 9>{}); break;
+    case 10: f(std::integral_constant<int, 10>{}); break;
+    case 11: f(std::integral_constant<int, 11>{}); break;
+    case 12: f(std::integral_constant<int, 12>{}); break;
+    default: return Status::shape("row kernels support hidden sizes up to 3072");
+  }
+  return Status::ok();
+}
+
 Status ln_modulate(const float* x, int rows, int ldx, const float* shift, const float* scale,
                    void* out, int ldo, bool out_bf16, const Geo& g, hipStream_t s) {
   if (rows <= 0) return Status::ok();
-  hipLaunchKernelGGL(k_ln_modulate, dim3((rows + 3) / 4), dim3(256), 0, s, x, rows, ldx, shift,
-                     scale, out, ldo, g.d, g.eps, out_bf16);
+  DC_TRY(with_nv(g.d, [&](auto nv) {
+    hipLaunchKernelGGL(k_ln_modulate<decltype(nv)::value>, dim3((rows + 3) / 4), dim3(256), 0, s, x,
+                       rows, ldx, shift, scale, out, ldo, g.d, g.eps, out_bf16);
+  }));
   DC_LAUNCH_CHECK();
   return Status::ok();
 }
@@ -321,16 +355,24 @@ Status cache_apply(const float* h_in, const void* resid, float* gout, const IdxL
 }
 
 Status drift(const float* h_in, const float* mod0, void* u_ref, bool snapshot, double* sums,
-             const IdxList& idx, const Geo& g, double* part, int32_t* cnt, hipStream_t s) {
+             const IdxList& idx, const Geo& g, double* part, hipStream_t s) {
   const int nblk = std::min(kDriftBlocks, (g.Nv + 3) / 4);
+  DC_TRY(with_nv(g.d, [&](auto nv) {
+    constexpr int NV = decltype(nv)::value;
+    if (g.bf16)
+      hipLaunchKernelGGL((k_drift<true, NV>), dim3(nblk, idx.n), dim3(256), 0, s, h_in, mod0, u_ref,
+                         snapshot ? 1 : 0, idx, g.Nv, g.d, size_t(g.N) * g.d, size_t(g.Nv) * g.d,
+                         g.eps, part);
+    else
+      hipLaunchKernelGGL((k_drift<false, NV>), dim3(nblk, idx.n), dim3(256), 0, s, h_in, mod0, u_ref,
+                         snapshot ? 1 : 0, idx, g.Nv, g.d, size_t(g.N) * g.d, size_t(g.Nv) * g.d,
+                         g.eps, part);
+  }));
+  DC_LAUNCH_CHECK();
   if (!snapshot) {
-    hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(DC_MAX_BATCH), 0, s, cnt, idx.n);
+    hipLaunchKernelGGL(k_drift_reduce, dim3(idx.n), dim3(256), 0, s, part, nblk, idx, sums);
     DC_LAUNCH_CHECK();
   }
-  hipLaunchKernelGGL(k_drift, dim3(nblk, idx.n), dim3(256), 0, s, h_in, mod0, u_ref,
-                     snapshot ? 1 : 0, sums, idx, g.Nv, g.d, size_t(g.N) * g.d,
-                     size_t(g.Nv) * g.d, g.eps, g.bf16, part, cnt);
-  DC_LAUNCH_CHECK();
   return Status::ok();
 }
 

@@ -121,7 +121,11 @@ def test_patch_embed(api, dev, name):
     got = h_in.cpu().numpy()
     P = dit.Params(W)
     want = dit.embed(P, x[1], txt[1])
-    assert rel_l2(got[1, : m.n_v], want[: m.n_v]) < 1e-6
+    # fp32 model: fp32 SIMT GEMM.  bf16 model: the fp32 operands are split into two
+    # bf16 terms each (16 significand bits), so about 2^-18 relative per product;
+    # the bf16 model's own bar is 1e-2 per block.
+    tol = 1e-5 if m.dtype == "bf16" else 1e-6
+    assert rel_l2(got[1, : m.n_v], want[: m.n_v]) < tol
     assert np.array_equal(got[1, m.n_v:], txt[1])
     assert not got[0].any()
 
