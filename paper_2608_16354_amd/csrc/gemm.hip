@@ -226,7 +226,13 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
 
   const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if (t >= tiles) return;
-  const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
+  // groups of four row tiles: consecutive tiles (the ones an XCD runs together)
+  // walk down a group before moving right, so their A and W k-slices share L2
+  const int tiles_m = (M + BM - 1) / BM;
+  const int grp = t / (4 * tiles_n), gbase = grp * 4;
+  const int gsz = min(4, tiles_m - gbase);
+  const int tin = t - grp * 4 * tiles_n;
+  const int m0 = (gbase + tin % gsz) * BM, n0 = (tin / gsz) * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
 
