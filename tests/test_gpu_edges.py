@@ -1,0 +1,153 @@
+"""Edge shapes of the device path against the oracle, through the C ABI.
+
+Small seeded models whose token counts leave ragged tails everywhere: fewer
+tokens than one attention tile (37, head_dim 72), fewer than one MFMA row tile
+and no text (16), one partial GEMM row tile (111), several row tiles, attention
+tiles and query blocks with a ragged last one (328), and the fp32 path at a
+ragged count (95).  Also: empty index lists leave every buffer untouched."""
+import numpy as np
+import pytest
+
+from oracle import dit, runtime
+from paper_2608_16354_amd import inputs as I
+from tests.gpu_util import mod_input, rel_l2, say, t
+from tests.test_gpu_kernels import _Head, _OneBlock
+
+pytestmark = pytest.mark.gpu
+
+
+def _shape(d, heads, hd, f, lat, n_txt, dtype):
+    return I.ModelShape(n_blocks=1, hidden=d, heads=heads, head_dim=hd, mlp_hidden=f, lat_c=16,
+                        lat_t=lat[0], lat_h=lat[1], lat_w=lat[2], patch=2, n_txt=n_txt, dtype=dtype)
+
+
+EDGE = {
+    "bf16-N37-hd72": (_shape(1152, 16, 72, 4608, (2, 6, 10), 7, "bf16"), 91),
+    "bf16-N16-notext": (_shape(256, 4, 64, 1024, (1, 8, 8), 0, "bf16"), 92),
+    "bf16-N111": (_shape(256, 4, 64, 1024, (3, 10, 12), 21, "bf16"), 93),
+    "bf16-N328": (_shape(384, 6, 64, 1536, (5, 14, 18), 13, "bf16"), 94),
+    "f32-N95": (_shape(256, 4, 64, 1024, (3, 10, 12), 5, "f32"), 95),
+}
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2608_16354_amd import api as A
+    A.L.load()
+    return A
+
+
+def _bf(m):
+    return m.dtype == "bf16"
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_block_forward(api, dev, name):
+    import torch
+    m, cid = EDGE[name]
+    W = I.Weights(m, cid)
+    dm = api.DeviceModel(_OneBlock(W, 0), dev)
+    ws = api.Workspace(m, 1, dev)
+    h = I.hidden_state(m, (40,))
+    mod = mod_input(m, (41,))
+    dh = t(h[None], dev)
+    say("edge block_forward", name, "N =", m.n_tok)
+    api.dc_block_forward(dm, 0, t(mod, dev), dh, [0], ws)
+    torch.cuda.synchronize()
+    got = dh[0].cpu().numpy()
+    want = dit.block(dit.Params(W), 0, mod.astype(np.float64), h.astype(np.float64))
+    err_h, err_d = rel_l2(got, want), rel_l2(got - h, want - h)
+    say(name, "block rel-L2 h_out", err_h, "update", err_d)
+    if _bf(m):
+        assert err_h < 1e-2 and err_d < 2e-2
+    else:
+        assert err_h < 1e-5 and err_d < 1e-5
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_patch_embed_and_head(api, dev, name):
+    import torch
+    m, cid = EDGE[name]
+    W = I.Weights(m, cid)
+    P = dit.Params(W)
+    dm = api.DeviceModel(_Head(W), dev)
+    ws = api.Workspace(m, 1, dev)
+    x = I.latent(m, cid, 0)
+    txt = I.text(m, cid, 0)
+    h_in = torch.zeros((1, m.n_tok, m.hidden), device=dev)
+    say("edge patch_embed", name, "N_v =", m.n_v)
+    api.dc_patch_embed(dm, t(x[None], dev), t(txt[None], dev), h_in, [0], ws)
+    torch.cuda.synchronize()
+    got = h_in[0].cpu().numpy()
+    want = dit.embed(P, x.astype(np.float64), txt)
+    assert rel_l2(got[: m.n_v], want[: m.n_v]) < (1e-5 if _bf(m) else 1e-6)
+    assert np.array_equal(got[m.n_v:], txt)
+    g = I.hidden_state(m, (42,))
+    hm = mod_input(m, (43,))[:2]
+    dx = t(x[None], dev)
+    say("edge head_euler", name)
+    api.dc_head_euler(dm, t(hm, dev), t(g[None], dev), dx, -0.02, [0], ws)
+    torch.cuda.synchronize()
+    v = dit.head(P, hm.astype(np.float64), g[: m.n_v].astype(np.float64))
+    want_x = dit.euler(x.astype(np.float64), v, 0.52, 0.5)
+    err = rel_l2(dx[0].cpu().numpy() - x, want_x - x)
+    say(name, "head update rel-L2", err)
+    assert err < (1e-2 if _bf(m) else 1e-5)
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_drift_and_cache(api, dev, name):
+    import torch
+    m, cid = EDGE[name]
+    cfg = api.model_cfg(m)
+    ws = api.Workspace(m, 1, dev)
+    mdt = torch.bfloat16 if _bf(m) else torch.float32
+    h_in = I.hidden_state(m, (44,))
+    mod0 = mod_input(m, (45,))[:2]
+    ref = I.normal((m.n_v, m.hidden), 1.0, (46,))
+    ref = I.round_bf16(ref) if _bf(m) else ref
+    u_ref = t(ref[None], dev, mdt)
+    sums = torch.zeros((1, 4), dtype=torch.float64, device=dev)
+    say("edge drift", name)
+    api.dc_drift_l1(cfg, t(h_in[None], dev), t(mod0, dev), u_ref, 0, sums, [0], ws)
+    torch.cuda.synchronize()
+    u = dit.modulate(h_in[: m.n_v].astype(np.float64), mod0[0].astype(np.float64),
+                     mod0[1].astype(np.float64), m.ln_eps)
+    want = runtime.drift_sums(u, ref.astype(np.float64))
+    assert np.allclose(sums[0].cpu().numpy(), want, rtol=2e-5)
+    h_out = h_in + I.normal(h_in.shape, 0.3, (47,))
+    resid = torch.zeros((1, m.n_v, m.hidden), dtype=mdt, device=dev)
+    say("edge cache_store", name)
+    api.dc_cache_store(cfg, t(h_out[None], dev), t(h_in[None], dev), resid, [0])
+    torch.cuda.synchronize()
+    exact = (h_out[: m.n_v].astype(np.float64) - h_in[: m.n_v]).astype(np.float32)
+    assert np.array_equal(resid[0].float().cpu().numpy(), I.round_bf16(exact) if _bf(m) else exact)
+
+
+def test_empty_index_lists_leave_buffers_untouched(api, dev):
+    """Every per-sample entry point with an empty index list is a no-op."""
+    import torch
+    m, cid = EDGE["bf16-N111"]
+    W = I.Weights(m, cid)
+    cfg = api.model_cfg(m)
+    dmb = api.DeviceModel(_OneBlock(W, 0), dev)
+    dmh = api.DeviceModel(_Head(W), dev)
+    ws = api.Workspace(m, 1, dev)
+    h = torch.full((1, m.n_tok, m.hidden), 3.0, device=dev)
+    x = torch.full((1, m.lat_c, m.lat_t, m.lat_h, m.lat_w), 5.0, device=dev)
+    txt = torch.zeros((1, m.n_txt, m.hidden), device=dev)
+    r = torch.full((1, m.n_v, m.hidden), 2.0, device=dev, dtype=torch.bfloat16)
+    g = torch.full((1, m.n_v, m.hidden), 4.0, device=dev)
+    sums = torch.full((1, 4), 6.0, dtype=torch.float64, device=dev)
+    mod = torch.zeros((6, m.hidden), device=dev)
+    say("empty index lists")
+    api.dc_patch_embed(dmh, x, txt, h, [], ws)
+    api.dc_block_forward(dmb, 0, mod, h, [], ws)
+    api.dc_cache_store(cfg, h, h, r, [])
+    api.dc_cache_apply(cfg, h, r, g, [])
+    api.dc_drift_l1(cfg, h, mod[:2], r, 0, sums, [], ws)
+    api.dc_drift_l1(cfg, h, mod[:2], r, 1, sums, [], ws)
+    api.dc_head_euler(dmh, mod[:2], g, x, 0.5, [], ws)
+    torch.cuda.synchronize()
+    assert (h == 3.0).all() and (x == 5.0).all() and (r.float() == 2.0).all()
+    assert (g == 4.0).all() and (sums == 6.0).all()
