@@ -2,8 +2,9 @@
 //
 // bf16 block GEMMs (QKV, out-projection, MLP up / down): v_mfma_f32_32x32x16_bf16,
 // 8 waves, block tile 256 x 192 x 64, tiles fed global -> LDS by LDS-DMA into two
-// stages, XOR-swizzled 128-byte rows, one barrier per k-step, XCD-aware tile
-// order; epilogues take one accumulator column at a time.
+// stages (the refill of the next k-step interleaved with this k-step's MFMAs),
+// XOR-swizzled 128-byte rows, one barrier per k-step, XCD-aware tile order;
+// epilogues take one accumulator column at a time.
 // bf16 head + Euler: a streaming kernel (A straight from HBM into MFMA
 // registers, the contraction split over the four waves of a workgroup).
 // bf16 patch embedding: fp32-accurate split-bf16 MFMA with the patchify gather fused.
@@ -200,14 +201,23 @@ struct EpiHeadEuler {
 // tile BM x BN x 64.  Tiles go global -> LDS with global_load_lds_dwordx4 (lane i
 // of an instruction lands at LDS base + 16 i, so the XOR swizzle is applied to the
 // global address each lane fetches): no staging registers and no LDS write
-// instructions.  Two stages in separate LDS arrays (so the compiler can tell
-// them apart and does not drain every load before each LDS read), one barrier
-// per k-step: the loads for step k+1 are issued right after it and overlap the
-// MFMAs of step k.  Rows past M or N are clamped to the last row (their results
-// are never stored).  Workgroups are renumbered so that each XCD (assigned
-// round-robin by workgroup id) processes a contiguous range of tiles.
+// instructions.  Two stages, one barrier per k-step: the loads for step k+1 are
+// issued two per 16-wide k-slice among the MFMAs of step k.  Rows past M or N
+// are clamped to the last row (their results are never stored).  Workgroups are
+// renumbered so that each XCD (assigned round-robin by workgroup id) processes a
+// contiguous range of tiles.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void;
+// 16 bytes per lane global -> LDS (global_load_lds_dwordx4): lane i's bytes land
+// at the wave-uniform LDS address dst + 16 i.  Issued as inline assembly so that
+// the compiler neither makes LDS reads of the other stage wait for it nor
+// reorders it; the kernel waits for its own fills (vmcnt) before each barrier.
+__device__ inline void dma16(const void* src, const void* dst) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst)));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(lds) : "memory", "m0");
+}
 
 template <int BM, int BN, int WM, int WN, class Epi>
 __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __restrict__ A, int lda,
@@ -250,18 +260,6 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
     const int r = slot >> 3, c = (slot & 7) ^ swz(slot >> 3);
     offB[i] = min(n0 + r, N - 1) * ldw + 8 * c;
   }
-  auto issue = [&](uint4* sa, uint4* sb, int kt) {
-    const int k0 = kt * BK;
-#pragma unroll
-    for (int i = 0; i < AI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(A + offA[i] + k0),
-                                       (lds_void*)(sa + (wave * AI + i) * 64), 16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < BI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(W + offB[i] + k0),
-                                       (lds_void*)(sb + (wave * BI + i) * 64), 16, 0, 0);
-  };
-
   f32x16 acc[TM][TN];
 #pragma unroll
   for (int a = 0; a < TM; ++a)
@@ -271,9 +269,25 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
       for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
 
   const int r32 = lane & 31, hi = lane >> 5;
-  auto compute = [&](const uint4* sa, const uint4* sb) {
+  // one DMA instruction (j < AI + BI) of the refill of stage (da, db) with k-step kt;
+  // compute() spreads the refill over its k-slices, two instructions per slice
+  auto dma_one = [&](uint4* da, uint4* db, int kt, int j) {
+    const int k0 = kt * BK;
+    if (j < AI) dma16(A + offA[j] + k0, da + (wave * AI + j) * 64);
+    else dma16(W + offB[j - AI] + k0, db + (wave * BI + (j - AI)) * 64);
+  };
+  auto compute = [&](const uint4* sa, const uint4* sb, uint4* da, uint4* db, int kt) {
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
+      if (kt >= 0) {
+#pragma unroll
+        for (int j = kk * 2; j < kk * 2 + 2; ++j)
+          if (j < AI + BI) dma_one(da, db, kt, j);
+        if (kk == BK / 16 - 1) {
+#pragma unroll
+          for (int j = 2 * (BK / 16); j < AI + BI; ++j) dma_one(da, db, kt, j);
+        }
+      }
       const int ch = kk * 2 + hi;
       bf16x8 af[TM], bf[TN];
 #pragma unroll
@@ -294,19 +308,18 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
     }
   };
 
-  const int KT = K / BK;
-  issue(sA0, sB0, 0);
+  const int KT = K / BK;                         // even: the launcher requires K % 128 == 0
+#pragma unroll
+  for (int j = 0; j < AI + BI; ++j) dma_one(sA0, sB0, 0, j);
   for (int kt = 0; kt < KT; kt += 2) {
-    // stage 0 holds k-step kt
-    __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave's loads landed
-    __builtin_amdgcn_s_barrier();                // everyone's landed; stage 1 is free
-    if (kt + 1 < KT) issue(sA1, sB1, kt + 1);
-    compute(sA0, sB0);
-    if (kt + 1 >= KT) break;
     __builtin_amdgcn_s_waitcnt(0x0F70);
-    __builtin_amdgcn_s_barrier();                // stage 0 is free
-    if (kt + 2 < KT) issue(sA0, sB0, kt + 2);
-    compute(sA1, sB1);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    compute(sA0, sB0, sA1, sB1, kt + 1);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    compute(sA1, sB1, sA0, sB0, kt + 2 < KT ? kt + 2 : -1);
   }
 
 #pragma unroll
@@ -323,7 +336,7 @@ template <int BM, int BN, int WM, int WN, class Epi>
 Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M, int N, int K,
                   const Epi& epi, hipStream_t s) {
   if (M <= 0) return Status::ok();
-  if (K % 64 || lda % 8 || ldw % 8) return Status::shape("bf16 GEMM needs K % 64 == 0 and 16-byte rows");
+  if (K % 128 || lda % 8 || ldw % 8) return Status::shape("bf16 GEMM needs K % 128 == 0 and 16-byte rows");
   if (int64_t(M) * lda > INT32_MAX || int64_t(N) * ldw > INT32_MAX)
     return Status::shape("bf16 GEMM operand exceeds 2^31 elements");
   const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
