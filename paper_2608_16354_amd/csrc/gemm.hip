@@ -5,8 +5,8 @@
 // stages (the refill of the next k-step interleaved with this k-step's MFMAs),
 // XOR-swizzled 128-byte rows, one barrier per k-step, XCD-aware tile order;
 // epilogues take one accumulator column at a time.
-// bf16 head + Euler: a streaming kernel (A straight from HBM into MFMA
-// registers, the contraction split over the four waves of a workgroup).
+// bf16 head + Euler: the same LDS-DMA GEMM with a 64 x 64 tile (N = 64 outputs)
+// and the unpatchify + Euler epilogue.
 // bf16 patch embedding: fp32-accurate split-bf16 MFMA with the patchify gather fused.
 // f32 path: a plain SIMT tiled kernel for the fp32 model and the small fp32
 // GEMMs (patch embedding of the fp32 model, timestep MLP).
@@ -173,6 +173,12 @@ struct EpiHeadEuler {
     const int c = n / pp, a = (n / p) % p, b = n % p;
     const int t = m / (Hp * Wp), i = (m / Wp) % Hp, j = m % Wp;
     return x + ((size_t(c) * T + t) * Hl + (p * i + a)) * Wl + (p * j + b);
+  }
+  __device__ void col(int mb, int n, int M, const f32x16& v) const {
+    float a[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) a[i] = v[i];
+    col(mb, n, M, a);
   }
   // rows mb + 8 (i / 4) + i % 4 of output column n: all loads, then all stores
   __device__ void col(int mb, int n, int M, const float (&v)[16]) const {
@@ -348,84 +354,6 @@ Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M,
   return Status::ok();
 }
 
-
-// ---------------------------------------------------------------------------
-// Head + Euler (bf16): x += dsigma * (A W^T + b) with A [M, d] bf16 (the
-// modulated final hidden state), W [64, d] bf16, scattered into the latent.
-// N = 64 outputs per token and each A element is used once, so the kernel
-// streams A straight from HBM into MFMA registers (no LDS staging).  A workgroup
-// owns 64 tokens; its four waves split d into quarters and each accumulates a
-// 64 x 64 partial; the partials meet in LDS and are added in wave order
-// (reproducible), each wave finishing one 32 x 32 output tile.
-// ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) k_head_bf16(const uint16_t* __restrict__ A, int lda,
-                                                   const uint16_t* __restrict__ W, int d, int M,
-                                                   EpiHeadEuler epi) {
-  __shared__ float part[4][4][16][64];     // [wave][tile][register][lane]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r32 = lane & 31, hi = lane >> 5;
-  const int m0 = blockIdx.x * 64;
-  const int kq = d >> 2, k0 = wave * kq;   // this wave's quarter of the contraction
-  const uint16_t* arow[2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a) arow[a] = A + size_t(min(m0 + 32 * a + r32, M - 1)) * lda + k0 + 8 * hi;
-  const uint16_t* wrow[2];
-#pragma unroll
-  for (int b = 0; b < 2; ++b) wrow[b] = W + size_t(32 * b + r32) * d + k0 + 8 * hi;
-  f32x16 acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
-  // groups of four 16-wide slices (kq is a multiple of 32), double-buffered:
-  // the loads of group g + 1 are in flight while group g is multiplied
-  bf16x8 af[2][4][2], bf[2][4][2];
-  auto load = [&](int buf, int k) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (k + 16 * j < kq) {
-#pragma unroll
-        for (int a = 0; a < 2; ++a) af[buf][j][a] = *reinterpret_cast<const bf16x8*>(arow[a] + k + 16 * j);
-#pragma unroll
-        for (int b = 0; b < 2; ++b) bf[buf][j][b] = *reinterpret_cast<const bf16x8*>(wrow[b] + k + 16 * j);
-      }
-  };
-  auto mma = [&](int buf, int k) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (k + 16 * j < kq) {
-#pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-          for (int b = 0; b < 2; ++b)
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[buf][j][a], bf[buf][j][b], acc[a][b], 0, 0, 0);
-      }
-  };
-  load(0, 0);
-  for (int k = 0; k < kq; k += 128) {
-    if (k + 64 < kq) load(1, k + 64);
-    mma(0, k);
-    if (k + 64 >= kq) break;
-    if (k + 128 < kq) load(0, k + 128);
-    mma(1, k + 64);
-  }
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) part[wave][t][i][lane] = acc[t >> 1][t & 1][i];
-  __syncthreads();
-  // wave w finishes output tile w: token rows 32 (w / 2) + ..., outputs 32 (w % 2) + r32
-  const int n = 32 * (wave & 1) + r32;
-  const int mb = m0 + 32 * (wave >> 1) + 4 * hi;
-  float v[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i)
-    v[i] = ((part[0][wave][i][lane] + part[1][wave][i][lane]) + part[2][wave][i][lane]) +
-           part[3][wave][i][lane];
-  epi.col(mb, n, M, v);
-}
 
 // ---------------------------------------------------------------------------
 // Patch embedding for the bf16 model: h_in[n] = patch(x)[n] W_pe^T + b + pos[n]
@@ -643,9 +571,7 @@ Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float
   if (M <= 0) return Status::ok();
   if (g.P != 64 || g.d % 128 || lda % 8) return Status::shape("bf16 head needs 64 outputs and d % 128 == 0");
   EpiHeadEuler e{bias, x, dsigma, g.T, g.Hl, g.Wl, g.p, g.Hp, g.Wp};
-  hipLaunchKernelGGL(k_head_bf16, dim3((M + 63) / 64), dim3(256), 0, s, A, lda, W, g.d, M, e);
-  DC_HIP(hipGetLastError());
-  return Status::ok();
+  return launch_dma<64, 64, 2, 2>(A, lda, W, g.d, M, 64, g.d, e, s);
 }
 
 Status patch_embed_bf16(const float* x, const float* W, const float* bias, const uint16_t* pos,
