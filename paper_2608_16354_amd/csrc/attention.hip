@@ -14,13 +14,14 @@
 // swapped) so that the eight scores a lane holds for each 16-token slice of P are
 // eight consecutive tokens: P goes from the score registers straight into the
 // B operand of the P V product, and V^T is read with one 16-byte LDS load.
-// Per-score VALU work is kept to the exponential, the bf16 conversion and half
-// a v_dot2 (the row sum adds pairs of bf16 P values): the subtraction of the
-// running maximum m rides on the MFMA as one extra rank-1 step (a column of ones
-// times -m).  m is set from the first tile's maximum and raised only when a
-// tile's P would grow past 2^64 (the tile's row sum, which the v_dot2 chain
-// yields anyway, is the test), so the common path takes no tile maximum; P and
-// the fp32 sums stay far inside the fp32 range either way.
+// Per-score VALU work is kept to the exponential, half a bf16 conversion and one
+// fp32 add for the row sum: the subtraction of the running maximum m rides on
+// the MFMA as one extra rank-1 step (a column of ones times -m).  The row sum is
+// a plain v_add chain rather than v_dot2 on the bf16 pairs: on gfx950 the dot
+// instructions do not issue alongside running MFMAs, adds do.  m is set from
+// the first tile's maximum and raised only when a tile's P would grow past 2^64
+// (the tile's row sum is the test), so the common path takes no tile maximum;
+// P and the fp32 sums stay far inside the fp32 range either way.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -49,17 +50,17 @@ __device__ inline int perm_kv(int m) { return (m & ~12) | ((m & 4) << 1) | ((m &
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// 16 bytes per lane global -> LDS (global_load_lds_dwordx4): lane i's bytes land
-// at the wave-uniform LDS address dst + 16 i.  Issued as inline assembly: the
-// compiler cannot tell the stage being filled from the stage being read and
-// would otherwise wait for every outstanding fill before each LDS read.  The
-// kernel waits for its own fills explicitly (vmcnt) before the barrier that
+// 16 bytes per lane global -> LDS (global_load_lds_dwordx4): lane i reads
+// base + off (a wave-uniform 64-bit base, a per-lane 32-bit byte offset) and its
+// bytes land at the wave-uniform LDS address dst + 16 i.  Issued as inline
+// assembly: the compiler cannot tell the stage being filled from the stage being
+// read and would otherwise wait for every outstanding fill before each LDS read.
+// The kernel waits for its own fills explicitly (vmcnt) before the barrier that
 // publishes a stage.
-__device__ inline void dma16(const void* src, const void* dst) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(
-      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst)));
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(lds) : "memory", "m0");
+__device__ inline void dma16(const void* base, uint32_t off, const void* dst) {
+  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
 }
 
 template <int D>
@@ -84,15 +85,23 @@ struct AttnShape {
 // padding chunks, V^T rows past D) fetch real, finite data whose products are
 // either multiplied by zero (padded Q columns, masked P) or never stored.
 template <int D>
-__global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ qk,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
+k_attn_bf16(const uint16_t* __restrict__ qk,
                                                    const uint16_t* __restrict__ vt, int ldv,
                                                    uint16_t* __restrict__ out, int M, int d,
                                                    int nqb, int items, int per_xcd) {
   using S = AttnShape<D>;
   constexpr int DK = S::DK, KC = S::KC, DC8 = S::DC8, TV = S::TV, BKV = S::BKV;
   constexpr int KI = S::KI, VI = S::VI;
-  __shared__ uint4 sK0[KI * 256], sK1[KI * 256], sK2[KI * 256];
-  __shared__ uint4 sV0[VI * 256], sV1[VI * 256], sV2[VI * 256];
+  // one array, so every stage address is a constant offset from one base
+  constexpr int STAGE = (KI + VI) * 256;
+  __shared__ uint4 lds[3 * STAGE];
+  uint4* const sK0 = lds;
+  uint4* const sV0 = lds + KI * 256;
+  uint4* const sK1 = lds + STAGE;
+  uint4* const sV1 = lds + STAGE + KI * 256;
+  uint4* const sK2 = lds + 2 * STAGE;
+  uint4* const sV2 = lds + 2 * STAGE + KI * 256;
 
   // Work item w = head * nqb + query block.  Workgroups are dealt to the XCDs
   // round-robin, so workgroup b runs item (b % 8) * per_xcd + b / 8: each XCD
@@ -101,7 +110,8 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if (w >= items) return;
   const int head = w / nqb;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: DMA addresses in SGPRs
   const int g = lane >> 5, r32 = lane & 31;
   const int q0 = (w - head * nqb) * 128 + wave * 32;
   const int ldq = 2 * d;
@@ -124,32 +134,32 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   // later wait on them can also hold up the tile pipeline
   __builtin_amdgcn_s_waitcnt(0x0F70);
 
-  // per-lane source offsets of this wave's DMA instructions for tile 0; tile t
+  // per-lane source byte offsets of this wave's DMA instructions for tile 0; tile t
   // adds a uniform t * 64 rows (K) or t * 64 columns (V^T).  K rows run up to
   // 64 + 12 past the tile start: the qk buffer has ldv + 64 rows, and rows past M
   // only feed scores that the last tile masks (by assignment, so any bits are safe).
-  int offK[KI], offV[VI];
+  uint32_t offK[KI], offV[VI];
 #pragma unroll
   for (int i = 0; i < KI; ++i) {
     const int slot = (wave * KI + i) * 64 + lane;
     const int r = slot / KC, pc = slot % KC;
     const int c = (KC == 8) ? (pc ^ swz_k(r)) : pc;
     const int cc = c < DC8 ? c : 0;                    // padding chunk: any real chunk
-    offK[i] = r * ldq + 8 * cc;
+    offK[i] = 2u * uint32_t(r * ldq + 8 * cc);
   }
 #pragma unroll
   for (int i = 0; i < VI; ++i) {
     const int slot = (wave * VI + i) * 64 + lane;
     const int r = slot >> 3, c = (slot & 7) ^ swz_v(slot >> 3);
-    offV[i] = min(r, D - 1) * ldv + 8 * c;
+    offV[i] = 2u * uint32_t(min(r, D - 1) * ldv + 8 * c);
   }
   auto issue = [&](uint4* sk, uint4* sv, int t) {
     const uint16_t* kt = Kb + size_t(t) * BKV * ldq;
     const uint16_t* vtt = Vb + t * BKV;
 #pragma unroll
-    for (int i = 0; i < KI; ++i) dma16(kt + offK[i], sk + (wave * KI + i) * 64);
+    for (int i = 0; i < KI; ++i) dma16(kt, offK[i], sk + (wave * KI + i) * 64);
 #pragma unroll
-    for (int i = 0; i < VI; ++i) dma16(vtt + offV[i], sv + (wave * VI + i) * 64);
+    for (int i = 0; i < VI; ++i) dma16(vtt, offV[i], sv + (wave * VI + i) * 64);
   };
 
   f32x16 o[TV];
@@ -165,8 +175,6 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   const s16x4 kaug = {short(g == 0 ? 0x3F80 : 0), 0, 0, 0};
   s16x4 qaug = {0, 0, 0, 0};
   float mrow = 0.f, lsum = 0.f;
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
   auto compute = [&](const uint4* sk, const uint4* sv, int t) {
     // S^T for two 32-token sub-tiles; sub-tile st, register i holds token
@@ -223,16 +231,17 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     bf16x8 pf[4];
     float ts = 0.f;
     auto exps = [&]() {
-      ts = 0.f;
+      // two add chains over the fp32 exponentials (the MFMA consumes them rounded to bf16)
+      float t2[2];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
+      for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[c][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[c >> 1][8 * (c & 1) + e]));
-        ts = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 0, 1), one2, ts, false);
-        ts = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 2, 3), one2, ts, false);
-        ts = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 4, 5), one2, ts, false);
-        ts = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[c], pf[c], 6, 7), one2, ts, false);
-      }
+        for (int e = 0; e < 8; ++e) {
+          const float p = __builtin_amdgcn_exp2f(s[c >> 1][8 * (c & 1) + e]);
+          t2[e & 1] = (c == 0 && e < 2) ? p : t2[e & 1] + p;
+          pf[c][e] = static_cast<__bf16>(p);
+        }
+      ts = t2[0] + t2[1];
     };
     exps();
     // P stays far inside fp32 range while m lags the running maximum by less than
