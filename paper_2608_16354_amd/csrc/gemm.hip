@@ -27,6 +27,7 @@ __device__ inline uint16_t to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 __device__ inline float from_bf16(uint16_t u) { return __uint_as_float(uint32_t(u) << 16); }
+inline bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 // LDS chunk swizzle for 128-byte tile rows.  gfx950's LDS serves 256 bytes per
 // cycle (64 banks), so two consecutive 128-byte rows share a bank cycle: keying
@@ -40,18 +41,46 @@ __device__ inline float gelu_tanh(float z) {
   const float y = 0.7978845608028654f * (z + 0.044715f * z * z * z);
   return z / (1.0f + __expf(-2.0f * y));
 }
+// the same with v_rcp_f32 (1 ulp) in place of the IEEE division, for bf16 outputs
+__device__ inline float gelu_tanh_fast(float z) {
+  const float y = 0.7978845608028654f * (z + 0.044715f * z * z * z);
+  return z * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * y));
+}
 __device__ inline float silu(float z) { return z / (1.0f + expf(-z)); }
 
 // ---------------------------------------------------------------------------
 // epilogues: operator()(m, n, acc) for one output element
 // ---------------------------------------------------------------------------
-// The MFMA GEMM hands its epilogue one accumulator column at a time: col(mb, n,
-// M, v) gets v[i] = C[mb + 8 (i / 4) + i % 4][n] for i < 16 (mb a multiple of 4),
-// so an epilogue can issue all of its loads for the column before any store.
+// The MFMA GEMM hands its epilogue either one accumulator column at a time: col(mb,
+// n, M, v) gets v[i] = C[mb + 8 (i / 4) + i % 4][n] for i < 16 (mb a multiple of 4),
+// or, when the epilogue declares kRowVec = V > 0, V consecutive columns of NP rows:
+// rows<NP>(m0, dm, n, M, v) gets v[k][j] = C[m0 + k dm][n + j] (n a multiple of V), so
+// it can issue all of its loads before any store; the GEMM transposes
+// each 32 x 32 accumulator tile through LDS for that, so the stores are 16 bytes
+// per lane instead of one element.  isrow(n) says whether the 32-column tile that
+// starts at n goes the row way (otherwise col).
 // Q (columns < d) leaves pre-multiplied by qscale = log2(e)/sqrt(d_h): the bf16
 // attention kernel takes its scores in log2 units.
 struct EpiQKVBf16 {
   const float* bias; uint16_t* qk; uint16_t* vt; int d; int ldv; float qscale;
+  static constexpr int kRowVec = 8;
+  __device__ bool isrow(int n) const { return n < 2 * d; }    // Q and K rows; V^T by column
+  bool rows_aligned() const { return al16(qk) && al16(bias) && d % 4 == 0; }
+  template <int NP>
+  __device__ void rows(int m0, int dm, int n, int M, const float (&v)[NP][8]) const {
+    const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
+    const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
+    const float sc = n < d ? qscale : 1.0f;
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+      uint4 pk;
+      pk.x = uint32_t(to_bf16((v[k][0] + b0.x) * sc)) | (uint32_t(to_bf16((v[k][1] + b0.y) * sc)) << 16);
+      pk.y = uint32_t(to_bf16((v[k][2] + b0.z) * sc)) | (uint32_t(to_bf16((v[k][3] + b0.w) * sc)) << 16);
+      pk.z = uint32_t(to_bf16((v[k][4] + b1.x) * sc)) | (uint32_t(to_bf16((v[k][5] + b1.y) * sc)) << 16);
+      pk.w = uint32_t(to_bf16((v[k][6] + b1.z) * sc)) | (uint32_t(to_bf16((v[k][7] + b1.w) * sc)) << 16);
+      if (m0 + k * dm < M) *reinterpret_cast<uint4*>(qk + size_t(m0 + k * dm) * 2 * d + n) = pk;
+    }
+  }
   __device__ void col(int mb, int n, int M, const f32x16& v) const {
     const float b = bias[n];
     if (n < 2 * d) {
@@ -100,6 +129,27 @@ struct EpiQKVF32 {
 };
 struct EpiGateResidual {
   const float* bias; const float* gate; float* h; int ldh;
+  static constexpr int kRowVec = 4;
+  __device__ bool isrow(int) const { return true; }
+  bool rows_aligned() const { return al16(h) && al16(bias) && al16(gate) && ldh % 4 == 0; }
+  // rows m0 + k * dm (k < NP), columns n .. n + 3: all loads of h, then all stores
+  template <int NP>
+  __device__ void rows(int m0, int dm, int n, int M, const float (&v)[NP][4]) const {
+    const float4 g = *reinterpret_cast<const float4*>(gate + n);
+    const float4 b = *reinterpret_cast<const float4*>(bias + n);
+    float4 o[NP];
+#pragma unroll
+    for (int k = 0; k < NP; ++k)
+      o[k] = *reinterpret_cast<const float4*>(h + size_t(min(m0 + k * dm, M - 1)) * ldh + n);
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+      o[k].x += g.x * (v[k][0] + b.x);
+      o[k].y += g.y * (v[k][1] + b.y);
+      o[k].z += g.z * (v[k][2] + b.z);
+      o[k].w += g.w * (v[k][3] + b.w);
+      if (m0 + k * dm < M) *reinterpret_cast<float4*>(h + size_t(m0 + k * dm) * ldh + n) = o[k];
+    }
+  }
   __device__ void col(int mb, int n, int M, const f32x16& v) const {
     const float g = gate[n], b = bias[n];
     float* __restrict__ p = h + size_t(mb) * ldh + n;
@@ -128,6 +178,25 @@ struct EpiGateResidual {
 };
 struct EpiGeluBf16 {
   const float* bias; uint16_t* out; int ldo;
+  static constexpr int kRowVec = 8;
+  __device__ bool isrow(int) const { return true; }
+  bool rows_aligned() const { return al16(out) && al16(bias) && ldo % 8 == 0; }
+  template <int NP>
+  __device__ void rows(int m0, int dm, int n, int M, const float (&v)[NP][8]) const {
+    const float4 b0 = *reinterpret_cast<const float4*>(bias + n);
+    const float4 b1 = *reinterpret_cast<const float4*>(bias + n + 4);
+    const float bb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+      uint32_t w[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[j] = uint32_t(to_bf16(gelu_tanh_fast(v[k][2 * j] + bb[2 * j]))) |
+               (uint32_t(to_bf16(gelu_tanh_fast(v[k][2 * j + 1] + bb[2 * j + 1]))) << 16);
+      if (m0 + k * dm < M)
+        *reinterpret_cast<uint4*>(out + size_t(m0 + k * dm) * ldo + n) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
   __device__ void col(int mb, int n, int M, const f32x16& v) const {
     const float b = bias[n];
     uint16_t* __restrict__ o = out + size_t(mb) * ldo + n;
@@ -168,6 +237,11 @@ struct EpiPatch {
 // Head + Euler: token m, patch-vector index n -> latent element; x += dsigma * (acc + b).
 struct EpiHeadEuler {
   const float* bias; float* x; float dsigma; int T, Hl, Wl, p, Hp, Wp;
+  static constexpr int kRowVec = 0;                 // scattered latent writes: by column
+  __device__ bool isrow(int) const { return false; }
+  bool rows_aligned() const { return false; }
+  template <int NP>
+  __device__ void rows(int, int, int, int, const float (&)[NP][4]) const {}
   __device__ float* at(int m, int n) const {
     const int pp = p * p;
     const int c = n / pp, a = (n / p) % p, b = n % p;
@@ -214,22 +288,23 @@ struct EpiHeadEuler {
 // contiguous range of tiles.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void;
-// 16 bytes per lane global -> LDS (global_load_lds_dwordx4): lane i's bytes land
-// at the wave-uniform LDS address dst + 16 i.  Issued as inline assembly so that
-// the compiler neither makes LDS reads of the other stage wait for it nor
-// reorders it; the kernel waits for its own fills (vmcnt) before each barrier.
-__device__ inline void dma16(const void* src, const void* dst) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(
-      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst)));
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(lds) : "memory", "m0");
+// 16 bytes per lane global -> LDS (global_load_lds_dwordx4): lane i reads
+// base + off (wave-uniform 64-bit base in SGPRs, per-lane 32-bit byte offset) and
+// its bytes land at the wave-uniform LDS address dst + 16 i.  Issued as inline
+// assembly so that the compiler neither makes LDS reads of the other stage wait
+// for it nor reorders it; the kernel waits for its own fills (vmcnt) before each
+// barrier.
+__device__ inline void dma16(const void* base, uint32_t off, const void* dst) {
+  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
 }
 
 template <int BM, int BN, int WM, int WN, class Epi>
 __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __restrict__ A, int lda,
                                                   const uint16_t* __restrict__ W, int ldw, int M,
                                                   int N, int K, int tiles_n, int tiles, int per_xcd,
-                                                  Epi epi) {
+                                                  int rows_ok, Epi epi) {
   constexpr int BK = 64;
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -237,8 +312,12 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
   constexpr int AI = BM * 8 / 64 / NW, BI = BN * 8 / 64 / NW;   // DMA instructions per wave
   static_assert(TM >= 1 && TN >= 1 && AI * NW * 64 == BM * 8 && BI * NW * 64 == BN * 8,
                 "tile shape");
-  __shared__ uint4 sA0[BM * 8], sA1[BM * 8];
-  __shared__ uint4 sB0[BN * 8], sB1[BN * 8];
+  // one array, so every stage address is a constant offset from one base
+  __shared__ uint4 lds[2 * (BM + BN) * 8];
+  uint4* const sA0 = lds;
+  uint4* const sB0 = lds + BM * 8;
+  uint4* const sA1 = lds + (BM + BN) * 8;
+  uint4* const sB1 = lds + (2 * BM + BN) * 8;
 
   const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if (t >= tiles) return;
@@ -249,22 +328,24 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
   const int gsz = min(4, tiles_m - gbase);
   const int tin = t - grp * 4 * tiles_n;
   const int m0 = (gbase + tin % gsz) * BM, n0 = (tin / gsz) * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: DMA addresses in SGPRs
   const int wm = wave % WM, wn = wave / WM;
 
-  // per-lane global element offsets of this wave's DMA instructions (k-step 0)
-  int offA[AI], offB[BI];            // element offsets (operands stay below 2^31 elements)
+  // per-lane global byte offsets of this wave's DMA instructions (k-step 0); the
+  // operands stay below 2^31 elements, so the byte offsets fit 32 bits
+  uint32_t offA[AI], offB[BI];
 #pragma unroll
   for (int i = 0; i < AI; ++i) {
     const int slot = (wave * AI + i) * 64 + lane;
     const int r = slot >> 3, c = (slot & 7) ^ swz(slot >> 3);
-    offA[i] = min(m0 + r, M - 1) * lda + 8 * c;
+    offA[i] = 2u * uint32_t(min(m0 + r, M - 1) * lda + 8 * c);
   }
 #pragma unroll
   for (int i = 0; i < BI; ++i) {
     const int slot = (wave * BI + i) * 64 + lane;
     const int r = slot >> 3, c = (slot & 7) ^ swz(slot >> 3);
-    offB[i] = min(n0 + r, N - 1) * ldw + 8 * c;
+    offB[i] = 2u * uint32_t(min(n0 + r, N - 1) * ldw + 8 * c);
   }
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -279,8 +360,8 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
   // compute() spreads the refill over its k-slices, two instructions per slice
   auto dma_one = [&](uint4* da, uint4* db, int kt, int j) {
     const int k0 = kt * BK;
-    if (j < AI) dma16(A + offA[j] + k0, da + (wave * AI + j) * 64);
-    else dma16(W + offB[j - AI] + k0, db + (wave * BI + (j - AI)) * 64);
+    if (j < AI) dma16(A + k0, offA[j], da + (wave * AI + j) * 64);
+    else dma16(W + k0, offB[j - AI], db + (wave * BI + (j - AI)) * 64);
   };
   auto compute = [&](const uint4* sa, const uint4* sb, uint4* da, uint4* db, int kt) {
 #pragma unroll
@@ -328,12 +409,43 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
     compute(sA1, sB1, sA0, sB0, kt + 2 < KT ? kt + 2 : -1);
   }
 
+  // Epilogue.  Row-vector epilogues: each 32 x 32 accumulator tile goes through a
+  // per-wave LDS buffer (rows of 40 floats: the two row groups a ds_write_b32 covers
+  // land 32 banks apart) and comes back as V consecutive columns of one row per lane.
+  constexpr int RV = Epi::kRowVec > 0 ? Epi::kRowVec : 4;
+  constexpr int kS = 40;
+  static_assert(Epi::kRowVec == 0 || sizeof(lds) >= NW * 32 * kS * sizeof(float), "epilogue LDS");
+  if constexpr (Epi::kRowVec > 0) {
+    __builtin_amdgcn_s_barrier();              // every wave is done with the last stage
+    asm volatile("" ::: "memory");
+  }
+  float* const st = reinterpret_cast<float*>(lds) + wave * 32 * kS;
 #pragma unroll
   for (int b = 0; b < TN; ++b) {
-    const int n = n0 + wn * WTN + b * 32 + r32;
-    if (n < N) {
+    const int nb = n0 + wn * WTN + b * 32;     // first column of the tile
+    if (nb >= N) continue;
+    if (Epi::kRowVec > 0 && rows_ok && nb + 32 <= N && epi.isrow(nb)) {
 #pragma unroll
-      for (int a = 0; a < TM; ++a) epi.col(m0 + wm * WTM + a * 32 + 4 * hi, n, M, acc[a][b]);
+      for (int a = 0; a < TM; ++a) {
+        const int mb = m0 + wm * WTM + a * 32;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) st[(8 * (i >> 2) + 4 * hi + (i & 3)) * kS + r32] = acc[a][b][i];
+        constexpr int LPR = 32 / RV, RPI = 64 / LPR, NP = 32 / RPI;   // lanes per row, rows per pass
+        const int r0 = lane / LPR, c = (lane % LPR) * RV;
+        float v[NP][RV];
+#pragma unroll
+        for (int k = 0; k < NP; ++k)
+#pragma unroll
+          for (int q = 0; q < RV; q += 4) {
+            const float4 t = *reinterpret_cast<const float4*>(st + (k * RPI + r0) * kS + c + q);
+            v[k][q] = t.x; v[k][q + 1] = t.y; v[k][q + 2] = t.z; v[k][q + 3] = t.w;
+          }
+        epi.template rows<NP>(mb + r0, RPI, nb + c, M, v);
+      }
+    } else {
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+        if (nb + r32 < N) epi.col(m0 + wm * WTM + a * 32 + 4 * hi, nb + r32, M, acc[a][b]);
     }
   }
 }
@@ -348,8 +460,10 @@ Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M,
   const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
   const int tiles = tn * tm;
   const int per = (tiles + 7) / 8;
+  // row-vector epilogue stores need 16-byte aligned rows; otherwise every tile goes by column
+  const int rows_ok = epi.rows_aligned() ? 1 : 0;
   hipLaunchKernelGGL((k_gemm_dma<BM, BN, WM, WN, Epi>), dim3(8 * per), dim3(WM * WN * 64), 0, s, A, lda, W,
-                     ldw, M, N, K, tn, tiles, per, epi);
+                     ldw, M, N, K, tn, tiles, per, rows_ok, epi);
   DC_HIP(hipGetLastError());
   return Status::ok();
 }
