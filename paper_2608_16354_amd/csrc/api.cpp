@@ -76,6 +76,10 @@ Workspace workspace_layout(const Geo& g, int batch) {
   w.patch = take(size_t(g.Nv) * 64 * 4);
   (void)batch;
   w.drift_part = take(size_t(DC_MAX_BATCH) * kDriftBlocks * 4 * sizeof(double));
+  // split-tail partials of the bf16 attention: up to 64 split items per XCD, two halves of
+  // 128 queries x (head_dim + 4) floats each
+  w.attn_part_bytes = g.bf16 ? size_t(8) * 64 * 2 * 128 * (g.Dh + 4) * sizeof(float) : 0;
+  w.attn_part = take(w.attn_part_bytes);
   w.tm_e = take(size_t(w.kTmax) * 256 * 4);
   w.tm_h = take(size_t(w.kTmax) * g.d * 4);
   w.tm_c = take(size_t(w.kTmax) * g.d * 4);
@@ -178,7 +182,10 @@ Status block_forward(const Geo& g, const dc_block_weights* bw, const float* mod,
       const uint16_t* wqkv = static_cast<const uint16_t*>(bw->w_qkv);
       { ProfScope ps(KClass::kLnModulate, s); DC_TRY(ln_modulate(hb, N, d, shift1, scale1, a, d, true, g, s)); }
       { ProfScope ps(KClass::kGemmQKV, s); DC_TRY(gemm_bf16_qkv(a, wqkv, bw->b_qkv, qk, vt, L.ldv, g, N, s)); }
-      { ProfScope ps(KClass::kAttention, s); DC_TRY(attention_bf16(qk, vt, L.ldv, o, g, N, s)); }
+      {
+        ProfScope ps(KClass::kAttention, s);
+        DC_TRY(attention_bf16(qk, vt, L.ldv, o, g, N, at<float>(ws, L.attn_part), L.attn_part_bytes, s));
+      }
       {
         ProfScope ps(KClass::kGemmOut, s);
         DC_TRY(gemm_bf16_gate_residual(o, d, static_cast<const uint16_t*>(bw->w_o), bw->b_o, gate1,

@@ -89,7 +89,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
 k_attn_bf16(const uint16_t* __restrict__ qk,
                                                    const uint16_t* __restrict__ vt, int ldv,
                                                    uint16_t* __restrict__ out, int M, int d,
-                                                   int nqb, int items, int per_xcd) {
+                                                   int nqb, int items, int per_xcd, int full,
+                                                   float* __restrict__ part) {
   using S = AttnShape<D>;
   constexpr int DK = S::DK, KC = S::KC, DC8 = S::DC8, TV = S::TV, BKV = S::BKV;
   constexpr int KI = S::KI, VI = S::VI;
@@ -107,8 +108,27 @@ k_attn_bf16(const uint16_t* __restrict__ qk,
   // round-robin, so workgroup b runs item (b % 8) * per_xcd + b / 8: each XCD
   // sweeps a contiguous range of items, i.e. the query blocks of one head at a
   // time, and that head's K and V stay in its L2.
-  const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (w >= items) return;
+  //
+  // Tail split: XCD x owns items [x per_xcd, (x + 1) per_xcd).  Its first `full`
+  // work units are whole items; every later item is split into two units, one per
+  // half of the key tiles, so the last (partial) round of resident workgroups runs
+  // half as long.  A split unit leaves its unnormalised output, running maximum and
+  // row sum in `part` (record si = x (per_xcd - full) + index among the XCD's split
+  // items); k_attn_combine merges the two halves.
+  const int xcd = blockIdx.x & 7, u = blockIdx.x >> 3;
+  const int ibeg = xcd * per_xcd, iend = min(items, ibeg + per_xcd);
+  const int nfull = min(full, iend - ibeg);
+  int w, half = -1;
+  if (u < nfull) {
+    w = ibeg + u;
+  } else {
+    w = ibeg + nfull + ((u - nfull) >> 1);
+    half = (u - nfull) & 1;
+  }
+  if (w >= iend) return;
+  const int ntile = (M + BKV - 1) / BKV;
+  const int tb = half == 1 ? ntile / 2 : 0;              // key tiles [tb, te)
+  const int te = half == 0 ? ntile / 2 : ntile;
   const int head = w / nqb;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: DMA addresses in SGPRs
@@ -227,7 +247,7 @@ k_attn_bf16(const uint16_t* __restrict__ qk,
 #pragma unroll
         for (int i = 0; i < 16; ++i) s[st][i] -= up;
     };
-    if (t == 0) raise(true);
+    if (t == tb) raise(true);
     bf16x8 pf[4];
     float ts = 0.f;
     auto exps = [&]() {
@@ -247,7 +267,7 @@ k_attn_bf16(const uint16_t* __restrict__ qk,
     // P stays far inside fp32 range while m lags the running maximum by less than
     // about 58 (log2 units); only then is m raised (rare), so no tile maximum is
     // taken on the common path
-    if (t > 0 && __builtin_amdgcn_ballot_w64(!(ts < 0x1p64f)) != 0) {
+    if (t > tb && __builtin_amdgcn_ballot_w64(!(ts < 0x1p64f)) != 0) {
       raise(false);
       exps();
     }
@@ -266,25 +286,44 @@ k_attn_bf16(const uint16_t* __restrict__ qk,
 
   // vmcnt(n) with the other counters left alone
   constexpr int kPerTile = KI + VI;
-  const int nkv = (M + BKV - 1) / BKV;
-  issue(sK0, sV0, 0);
-  if (nkv > 1) issue(sK1, sV1, 1);
+  issue(sK0, sV0, tb);
+  if (tb + 1 < te) issue(sK1, sV1, tb + 1);
   auto step = [&](uint4* sk, uint4* sv, uint4* nk, uint4* nv, int t) {
-    if (t + 1 < nkv) __builtin_amdgcn_s_waitcnt(0x0F70 | kPerTile);   // tile t landed (t+1 may fly)
+    if (t + 1 < te) __builtin_amdgcn_s_waitcnt(0x0F70 | kPerTile);    // tile t landed (t+1 may fly)
     else __builtin_amdgcn_s_waitcnt(0x0F70);
     __builtin_amdgcn_s_barrier();          // everyone's tile t landed; tile t-1's stage is free
-    if (t + 2 < nkv) issue(nk, nv, t + 2);
+    if (t + 2 < te) issue(nk, nv, t + 2);
     compute(sk, sv, t);
   };
-  for (int t = 0; t < nkv; t += 3) {
+  for (int t = tb; t < te; t += 3) {
     step(sK0, sV0, sK2, sV2, t);
-    if (t + 1 >= nkv) break;
+    if (t + 1 >= te) break;
     step(sK1, sV1, sK0, sV0, t + 1);
-    if (t + 2 >= nkv) break;
+    if (t + 2 >= te) break;
     step(sK2, sV2, sK1, sV1, t + 2);
   }
 
   lsum += __shfl_xor(lsum, 32, 64);
+  if (half >= 0) {
+    // split unit: unnormalised O, m and l of the wave's 32 queries; record layout
+    // [half][128 queries][D + 4] floats (O, m, l, two unused: 16-byte aligned rows)
+    const int si = xcd * (per_xcd - full) + (w - ibeg - nfull);
+    float* rec = part + (size_t(si) * 2 + half) * 128 * (D + 4) + size_t(wave * 32 + r32) * (D + 4);
+#pragma unroll
+    for (int tv = 0; tv < TV; ++tv)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int dh = 32 * tv + 8 * i4 + 4 * g;
+        if (dh < D)
+          *reinterpret_cast<float4*>(rec + dh) =
+              make_float4(o[tv][4 * i4 + 0], o[tv][4 * i4 + 1], o[tv][4 * i4 + 2], o[tv][4 * i4 + 3]);
+      }
+    if (g == 0) {
+      rec[D] = mrow;
+      rec[D + 1] = lsum;
+    }
+    return;
+  }
   const float inv = 1.0f / lsum;
   const int q = q0 + r32;
   if (q < M) {
@@ -303,6 +342,42 @@ k_attn_bf16(const uint16_t* __restrict__ qk,
           *reinterpret_cast<ushort4*>(orow + dh) = u;
         }
       }
+  }
+}
+
+// Merge the two key halves of every split item: O = (O0 2^(m0-m) + O1 2^(m1-m)) /
+// (l0 2^(m0-m) + l1 2^(m1-m)) with m = max(m0, m1).  One workgroup per split item,
+// two threads per query (half of the head dimension each).
+template <int D>
+__global__ void __launch_bounds__(256) k_attn_combine(const float* __restrict__ part,
+                                                      uint16_t* __restrict__ out, int M, int d,
+                                                      int nqb, int items, int per_xcd, int full) {
+  const int per = per_xcd - full;                 // split items per XCD (record stride)
+  const int si = blockIdx.x, xcd = si / per, k = si % per;
+  const int ibeg = xcd * per_xcd, iend = min(items, ibeg + per_xcd);
+  const int w = ibeg + full + k;
+  if (full >= iend - ibeg || w >= iend) return;
+  const int head = w / nqb, ql = threadIdx.x >> 1, hf = threadIdx.x & 1;
+  const int q = (w - head * nqb) * 128 + ql;
+  if (q >= M) return;
+  const float* r0 = part + (size_t(si) * 2 + 0) * 128 * (D + 4) + size_t(ql) * (D + 4);
+  const float* r1 = r0 + 128 * (D + 4);
+  const float m0 = r0[D], l0 = r0[D + 1], m1 = r1[D], l1 = r1[D + 1];
+  const float m = fmaxf(m0, m1);
+  const float a0 = __builtin_amdgcn_exp2f(m0 - m), a1 = __builtin_amdgcn_exp2f(m1 - m);
+  const float inv = 1.0f / (l0 * a0 + l1 * a1);
+  constexpr int DH = D / 2;                       // 32 or 36 dims per thread
+  uint16_t* orow = out + size_t(q) * d + head * D + hf * DH;
+#pragma unroll
+  for (int j = 0; j < DH; j += 4) {
+    const float4 x0 = *reinterpret_cast<const float4*>(r0 + hf * DH + j);
+    const float4 x1 = *reinterpret_cast<const float4*>(r1 + hf * DH + j);
+    ushort4 v;
+    v.x = to_bf16((x0.x * a0 + x1.x * a1) * inv);
+    v.y = to_bf16((x0.y * a0 + x1.y * a1) * inv);
+    v.z = to_bf16((x0.z * a0 + x1.z * a1) * inv);
+    v.w = to_bf16((x0.w * a0 + x1.w * a1) * inv);
+    *reinterpret_cast<ushort4*>(orow + j) = v;
   }
 }
 
@@ -360,26 +435,58 @@ __global__ void __launch_bounds__(64) k_attn_f32(const float* __restrict__ qk,
 
 }  // namespace
 
+// Resident workgroups of the bf16 attention kernel per XCD on the current device
+// (compute units / 8 x workgroups per compute unit), cached per device.
+template <int D>
+static int attn_slots_per_xcd() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cache[dev] == 0) {
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_attn_bf16<D>, 256, 0) != hipSuccess)
+      return 0;
+    cache[dev] = (cus / 8) * per_cu;
+  }
+  return cache[dev];
+}
+
+template <int D>
+static Status launch_attn(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t* out, const Geo& g,
+                          int M, float* part, size_t part_bytes, hipStream_t s) {
+  const int nqb = (M + 127) / 128, items = nqb * g.H, per_xcd = (items + 7) / 8;
+  // split the items of the last partial round when their halves fit in one round
+  const int slots = attn_slots_per_xcd<D>();
+  int full = per_xcd;
+  if (slots > 0 && (M + 63) / 64 >= 2) {
+    const int f = per_xcd / slots * slots, r = per_xcd - f;
+    const size_t need = size_t(8) * r * 2 * 128 * (D + 4) * sizeof(float);
+    if (r > 0 && 2 * r <= slots && part && need <= part_bytes) full = f;
+  }
+  const int units = full + 2 * (per_xcd - full);
+  hipLaunchKernelGGL(k_attn_bf16<D>, dim3(8 * units), dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb,
+                     items, per_xcd, full, part);
+  DC_HIP(hipGetLastError());
+  if (full < per_xcd) {
+    hipLaunchKernelGGL(k_attn_combine<D>, dim3(8 * (per_xcd - full)), dim3(256), 0, s, part, out, M, g.d,
+                       nqb, items, per_xcd, full);
+    DC_HIP(hipGetLastError());
+  }
+  return Status::ok();
+}
+
 Status attention_bf16(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t* out,
-                      const Geo& g, int M, hipStream_t s) {
+                      const Geo& g, int M, float* part, size_t part_bytes, hipStream_t s) {
   if (ldv % 64 || ldv < M) return Status::shape("attention needs ldv >= M, ldv % 64 == 0");
   if (ldv > M) {
     uint16_t* v = const_cast<uint16_t*>(vt);
     hipLaunchKernelGGL(k_zero_vt_tail, dim3(64), dim3(256), 0, s, v, g.d, ldv, M);
     DC_HIP(hipGetLastError());
   }
-  const int nqb = (M + 127) / 128, items = nqb * g.H, per_xcd = (items + 7) / 8;
-  const dim3 grid(8 * per_xcd);
-  if (g.Dh == 64)
-    hipLaunchKernelGGL(k_attn_bf16<64>, grid, dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb, items,
-                       per_xcd);
-  else if (g.Dh == 72)
-    hipLaunchKernelGGL(k_attn_bf16<72>, grid, dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb, items,
-                       per_xcd);
-  else
-    return Status::shape("bf16 attention supports head_dim 64 and 72");
-  DC_HIP(hipGetLastError());
-  return Status::ok();
+  if (g.Dh == 64) return launch_attn<64>(qk, vt, ldv, out, g, M, part, part_bytes, s);
+  if (g.Dh == 72) return launch_attn<72>(qk, vt, ldv, out, g, M, part, part_bytes, s);
+  return Status::shape("bf16 attention supports head_dim 64 and 72");
 }
 
 Status attention_f32(const float* qk, const float* vt, int ldv, float* out, const Geo& g, int M,

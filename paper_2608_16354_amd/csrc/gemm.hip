@@ -282,7 +282,8 @@ struct EpiHeadEuler {
 // of an instruction lands at LDS base + 16 i, so the XOR swizzle is applied to the
 // global address each lane fetches): no staging registers and no LDS write
 // instructions.  Two stages, one barrier per k-step: the loads for step k+1 are
-// issued two per 16-wide k-slice among the MFMAs of step k.  Rows past M or N
+// issued among the MFMAs of the first DS 16-wide k-slices of step k (the block
+// GEMMs use DS = 2, so the last refill has half a step to land).  Rows past M or N
 // are clamped to the last row (their results are never stored).  Workgroups are
 // renumbered so that each XCD (assigned round-robin by workgroup id) processes a
 // contiguous range of tiles.
@@ -300,7 +301,64 @@ __device__ inline void dma16(const void* base, uint32_t off, const void* dst) {
                :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
 }
 
-template <int BM, int BN, int WM, int WN, class Epi>
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding: vmcnt bits
+// [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8])
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+constexpr int kEpiStride = 40;   // floats per row of the epilogue's per-wave LDS transpose buffer
+
+// Epilogue of the bf16 block GEMMs.  Row-vector epilogues: each 32 x 32
+// accumulator tile goes through a per-wave LDS buffer (rows of 40 floats: the two
+// row groups a ds_write_b32 covers land 32 banks apart) and comes back as V
+// consecutive columns of one row per lane.  The caller has finished every read of
+// the LDS stages (the barrier here orders the reuse).
+template <int BM, int BN, int WM, int WN, class Epi, int TM, int TN>
+__device__ inline void gemm_epilogue(f32x16 (&acc)[TM][TN], uint4* lds, int m0, int n0, int M,
+                                     int N, int wave, int lane, int rows_ok, const Epi& epi) {
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int RV = Epi::kRowVec > 0 ? Epi::kRowVec : 4;
+  constexpr int kS = kEpiStride;
+  const int wm = wave % WM, wn = wave / WM;
+  const int r32 = lane & 31, hi = lane >> 5;
+  if constexpr (Epi::kRowVec > 0) {
+    __builtin_amdgcn_s_barrier();              // every wave is done with the last stage
+    asm volatile("" ::: "memory");
+  }
+  float* const st = reinterpret_cast<float*>(lds) + wave * 32 * kS;
+#pragma unroll
+  for (int b = 0; b < TN; ++b) {
+    const int nb = n0 + wn * WTN + b * 32;     // first column of the tile
+    if (nb >= N) continue;
+    if (Epi::kRowVec > 0 && rows_ok && nb + 32 <= N && epi.isrow(nb)) {
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int mb = m0 + wm * WTM + a * 32;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) st[(8 * (i >> 2) + 4 * hi + (i & 3)) * kS + r32] = acc[a][b][i];
+        constexpr int LPR = 32 / RV, RPI = 64 / LPR, NP = 32 / RPI;   // lanes per row, rows per pass
+        const int r0 = lane / LPR, c = (lane % LPR) * RV;
+        float v[NP][RV];
+#pragma unroll
+        for (int k = 0; k < NP; ++k)
+#pragma unroll
+          for (int q = 0; q < RV; q += 4) {
+            const float4 t = *reinterpret_cast<const float4*>(st + (k * RPI + r0) * kS + c + q);
+            v[k][q] = t.x; v[k][q + 1] = t.y; v[k][q + 2] = t.z; v[k][q + 3] = t.w;
+          }
+        epi.template rows<NP>(mb + r0, RPI, nb + c, M, v);
+      }
+    } else {
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+        if (nb + r32 < N) epi.col(m0 + wm * WTM + a * 32 + 4 * hi, nb + r32, M, acc[a][b]);
+    }
+  }
+}
+
+template <int BM, int BN, int WM, int WN, int DS, class Epi>
 __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __restrict__ A, int lda,
                                                   const uint16_t* __restrict__ W, int ldw, int M,
                                                   int N, int K, int tiles_n, int tiles, int per_xcd,
@@ -355,9 +413,11 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
 
+  const int KT = K / BK;                         // even: the launcher requires K % 128 == 0
+
   const int r32 = lane & 31, hi = lane >> 5;
   // one DMA instruction (j < AI + BI) of the refill of stage (da, db) with k-step kt;
-  // compute() spreads the refill over its k-slices, two instructions per slice
+  // compute() spreads the refill over its first DS k-slices
   auto dma_one = [&](uint4* da, uint4* db, int kt, int j) {
     const int k0 = kt * BK;
     if (j < AI) dma16(A + k0, offA[j], da + (wave * AI + j) * 64);
@@ -367,13 +427,11 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       if (kt >= 0) {
+        // the refill goes out over the first DS k-slices, DPS instructions per slice
+        constexpr int DPS = (AI + BI + DS - 1) / DS;
 #pragma unroll
-        for (int j = kk * 2; j < kk * 2 + 2; ++j)
-          if (j < AI + BI) dma_one(da, db, kt, j);
-        if (kk == BK / 16 - 1) {
-#pragma unroll
-          for (int j = 2 * (BK / 16); j < AI + BI; ++j) dma_one(da, db, kt, j);
-        }
+        for (int j = kk * DPS; j < (kk + 1) * DPS; ++j)
+          if (j < AI + BI && kk < DS) dma_one(da, db, kt, j);
       }
       const int ch = kk * 2 + hi;
       bf16x8 af[TM], bf[TN];
@@ -395,62 +453,25 @@ __global__ void __launch_bounds__(WM * WN * 64) k_gemm_dma(const uint16_t* __res
     }
   };
 
-  const int KT = K / BK;                         // even: the launcher requires K % 128 == 0
 #pragma unroll
   for (int j = 0; j < AI + BI; ++j) dma_one(sA0, sB0, 0, j);
+  // before each barrier: this wave's refill has landed
   for (int kt = 0; kt < KT; kt += 2) {
-    __builtin_amdgcn_s_waitcnt(0x0F70);
+    wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     compute(sA0, sB0, sA1, sB1, kt + 1);
-    __builtin_amdgcn_s_waitcnt(0x0F70);
+    wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     compute(sA1, sB1, sA0, sB0, kt + 2 < KT ? kt + 2 : -1);
   }
 
-  // Epilogue.  Row-vector epilogues: each 32 x 32 accumulator tile goes through a
-  // per-wave LDS buffer (rows of 40 floats: the two row groups a ds_write_b32 covers
-  // land 32 banks apart) and comes back as V consecutive columns of one row per lane.
-  constexpr int RV = Epi::kRowVec > 0 ? Epi::kRowVec : 4;
-  constexpr int kS = 40;
-  static_assert(Epi::kRowVec == 0 || sizeof(lds) >= NW * 32 * kS * sizeof(float), "epilogue LDS");
-  if constexpr (Epi::kRowVec > 0) {
-    __builtin_amdgcn_s_barrier();              // every wave is done with the last stage
-    asm volatile("" ::: "memory");
-  }
-  float* const st = reinterpret_cast<float*>(lds) + wave * 32 * kS;
-#pragma unroll
-  for (int b = 0; b < TN; ++b) {
-    const int nb = n0 + wn * WTN + b * 32;     // first column of the tile
-    if (nb >= N) continue;
-    if (Epi::kRowVec > 0 && rows_ok && nb + 32 <= N && epi.isrow(nb)) {
-#pragma unroll
-      for (int a = 0; a < TM; ++a) {
-        const int mb = m0 + wm * WTM + a * 32;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) st[(8 * (i >> 2) + 4 * hi + (i & 3)) * kS + r32] = acc[a][b][i];
-        constexpr int LPR = 32 / RV, RPI = 64 / LPR, NP = 32 / RPI;   // lanes per row, rows per pass
-        const int r0 = lane / LPR, c = (lane % LPR) * RV;
-        float v[NP][RV];
-#pragma unroll
-        for (int k = 0; k < NP; ++k)
-#pragma unroll
-          for (int q = 0; q < RV; q += 4) {
-            const float4 t = *reinterpret_cast<const float4*>(st + (k * RPI + r0) * kS + c + q);
-            v[k][q] = t.x; v[k][q + 1] = t.y; v[k][q + 2] = t.z; v[k][q + 3] = t.w;
-          }
-        epi.template rows<NP>(mb + r0, RPI, nb + c, M, v);
-      }
-    } else {
-#pragma unroll
-      for (int a = 0; a < TM; ++a)
-        if (nb + r32 < N) epi.col(m0 + wm * WTM + a * 32 + 4 * hi, nb + r32, M, acc[a][b]);
-    }
-  }
+  static_assert(Epi::kRowVec == 0 || sizeof(lds) >= NW * 32 * kEpiStride * sizeof(float), "epilogue LDS");
+  gemm_epilogue<BM, BN, WM, WN>(acc, lds, m0, n0, M, N, wave, lane, rows_ok, epi);
 }
 
-template <int BM, int BN, int WM, int WN, class Epi>
+template <int BM, int BN, int WM, int WN, int DS, class Epi>
 Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M, int N, int K,
                   const Epi& epi, hipStream_t s) {
   if (M <= 0) return Status::ok();
@@ -462,7 +483,7 @@ Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M,
   const int per = (tiles + 7) / 8;
   // row-vector epilogue stores need 16-byte aligned rows; otherwise every tile goes by column
   const int rows_ok = epi.rows_aligned() ? 1 : 0;
-  hipLaunchKernelGGL((k_gemm_dma<BM, BN, WM, WN, Epi>), dim3(8 * per), dim3(WM * WN * 64), 0, s, A, lda, W,
+  hipLaunchKernelGGL((k_gemm_dma<BM, BN, WM, WN, DS, Epi>), dim3(8 * per), dim3(WM * WN * 64), 0, s, A, lda, W,
                      ldw, M, N, K, tn, tiles, per, rows_ok, epi);
   DC_HIP(hipGetLastError());
   return Status::ok();
@@ -663,7 +684,7 @@ Status gemm_f32_qkv(const float* A, const float* W, const float* bias, float* qk
 
 Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, uint16_t* qk,
                      uint16_t* vt, int ldv, const Geo& g, int M, hipStream_t s) {
-  return launch_dma<256, 192, 4, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
+  return launch_dma<256, 192, 4, 2, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
                                     EpiQKVBf16{bias, qk, vt, g.d, ldv,
                                                float(1.4426950408889634 / std::sqrt(double(g.Dh)))},
                                     s);
@@ -672,12 +693,12 @@ Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, ui
 Status gemm_bf16_gate_residual(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
                                const float* gate, float* h, int ldh, int M, int N, int K,
                                hipStream_t s) {
-  return launch_dma<256, 192, 4, 2>(A, lda, W, K, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
+  return launch_dma<256, 192, 4, 2, 2>(A, lda, W, K, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
 }
 
 Status gemm_bf16_gelu(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
                       uint16_t* out, int ldo, int M, int N, int K, hipStream_t s) {
-  return launch_dma<256, 192, 4, 2>(A, lda, W, K, M, N, K, EpiGeluBf16{bias, out, ldo}, s);
+  return launch_dma<256, 192, 4, 2, 2>(A, lda, W, K, M, N, K, EpiGeluBf16{bias, out, ldo}, s);
 }
 
 Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float* bias, float* x,
@@ -685,7 +706,7 @@ Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float
   if (M <= 0) return Status::ok();
   if (g.P != 64 || g.d % 128 || lda % 8) return Status::shape("bf16 head needs 64 outputs and d % 128 == 0");
   EpiHeadEuler e{bias, x, dsigma, g.T, g.Hl, g.Wl, g.p, g.Hp, g.Wp};
-  return launch_dma<64, 64, 2, 2>(A, lda, W, g.d, M, 64, g.d, e, s);
+  return launch_dma<64, 64, 2, 2, 4>(A, lda, W, g.d, M, 64, g.d, e, s);
 }
 
 Status patch_embed_bf16(const float* x, const float* W, const float* bias, const uint16_t* pos,

@@ -92,7 +92,7 @@ Status make_idx(const int32_t* idx, int32_t n, IdxList& out);
 
 // Workspace layout (offsets in bytes, each 256-aligned).
 struct Workspace {
-  size_t a, qk, vt, o, ff, patch, drift_part, tm_e, tm_h, tm_c, tm_s, tm_m, total;
+  size_t a, qk, vt, o, ff, patch, drift_part, attn_part, attn_part_bytes, tm_e, tm_h, tm_c, tm_s, tm_m, total;
   int ldv;               // row stride of the transposed value buffer (tokens, padded)
   int kTmax;             // steps the modulation scratch can hold per pass
 };
@@ -135,8 +135,10 @@ Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float
                       float dsigma, const Geo& g, int M, hipStream_t s);
 
 // Attention over one sample: qk [M, 2d] (Q | K), vt [heads][Dh][ldv], out [M, d].
+// part: scratch for the split tail items (unnormalised partial outputs), part_bytes its size;
+// with too little scratch the tail is not split.
 Status attention_bf16(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t* out,
-                      const Geo& g, int M, hipStream_t s);
+                      const Geo& g, int M, float* part, size_t part_bytes, hipStream_t s);
 Status attention_f32(const float* qk, const float* vt, int ldv, float* out, const Geo& g, int M,
                      hipStream_t s);
 

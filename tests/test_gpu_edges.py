@@ -3,8 +3,11 @@
 Small seeded models whose token counts leave ragged tails everywhere: fewer
 tokens than one attention tile (37, head_dim 72), fewer than one MFMA row tile
 and no text (16), one partial GEMM row tile (111), several row tiles, attention
-tiles and query blocks with a ragged last one (328), and the fp32 path at a
-ragged count (95).  Also: empty index lists leave every buffer untouched."""
+tiles and query blocks with a ragged last one (328), the fp32 path at a
+ragged count (95), and 3,597 tokens x 30 heads, where the attention's query
+blocks outnumber the resident workgroups by just over three rounds on MI355X, so
+the last partial round runs as split key halves merged by the combine kernel.
+Also: empty index lists leave every buffer untouched."""
 import numpy as np
 import pytest
 
@@ -27,6 +30,7 @@ EDGE = {
     "bf16-N111": (_shape(256, 4, 64, 1024, (3, 10, 12), 21, "bf16"), 93),
     "bf16-N328": (_shape(384, 6, 64, 1536, (5, 14, 18), 13, "bf16"), 94),
     "f32-N95": (_shape(256, 4, 64, 1024, (3, 10, 12), 5, "f32"), 95),
+    "bf16-N3597-h30-split": (_shape(1920, 30, 64, 7680, (10, 32, 44), 77, "bf16"), 96),
 }
 
 
