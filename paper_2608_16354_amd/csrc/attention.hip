@@ -1,7 +1,10 @@
 // Joint video + text self-attention, softmax(Q K^T / sqrt(d_h)) V per head, with
 // an online softmax (flash-style: the N x N score matrix never leaves registers).
 //
-// bf16 path (gfx950 MFMA 32x32x16).  A workgroup is 4 waves x 32 query rows of one
+// Two bf16 kernels: k_attn16 (head_dim 64, sequences of 8,192 tokens and more; see its
+// own comment below) and k_attn_bf16 (head_dim 64 below that, and head_dim 72).
+//
+// k_attn_bf16 (gfx950 MFMA 32x32x16).  A workgroup is 4 waves x 32 query rows of one
 // head; key/value tiles of 64 tokens stream through a 3-stage LDS ring.  The QKV
 // GEMM stores Q pre-multiplied by log2(e)/sqrt(d_h), so scores arrive in log2
 // units and P = 2^(s - m).  Each wave
@@ -25,6 +28,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -381,6 +385,313 @@ __global__ void __launch_bounds__(256) k_attn_combine(const float* __restrict__ 
   }
 }
 
+// ---------------------------------------------------------------------------
+// head_dim 64 on v_mfma_f32_16x16x32_bf16.  Same work items, tail split and K/V^T
+// LDS ring as k_attn_bf16.  Per wave: 32 queries as two 16-query
+// blocks; the transposed scores S^T come in 16 x 16 blocks (lane: query lane % 16,
+// rows 4 (lane / 16) .. + 3 of the block).
+//  - The running maximum enters as the C operand of the first score MFMA (four
+//    registers holding -m per query block), so scores arrive as s - m.
+//  - Each lane's eight P values of a 32-key chunk are the B operand of
+//    O^T += V^T P^T directly (K rows permuted, see perm16); the matching V^T operand
+//    is one 16-byte LDS read.
+//  - The row sum l is one more MFMA per chunk with an all-ones A operand, so the
+//    VALU does one exp2 and half a bf16 pack per score and nothing else; numerator
+//    and denominator use the same bf16-rounded P.
+//  - m comes from the first tile's maximum and stays there.  When a tile leaves l at
+//    2^64 or more, or not finite (a later score more than about 58 above m), the whole
+//    workgroup redoes the item with the tile maximum taken on every tile (the safe
+//    pass); until then every P is below 2^64, so O cannot overflow.
+// ---------------------------------------------------------------------------
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// K rows are read in a permuted order within each 32-key chunk: S^T block row
+// 16 h + 4 g + i (h < 2, g < 4, i < 4) holds key 8 g + 4 h + i, so the eight P values
+// a lane holds for a chunk (rows 4 g + i of blocks 2c and 2c+1) are keys 8 g .. 8 g + 7
+// and the V^T operand is one 16-byte read.  The K swizzle is keyed on the row bits
+// that vary across the 16 rows one LDS cycle reads in that order.
+__device__ inline int perm16(int p) {
+  return (p & 32) | (((p >> 2) & 3) << 3) | (((p >> 4) & 1) << 2) | (p & 3);
+}
+__device__ inline int swz_k16(int row) { return ((row >> 1) & 1) | ((row >> 2) & 6); }
+
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+k_attn16(const uint16_t* __restrict__ qk, const uint16_t* __restrict__ vt, int ldv,
+         uint16_t* __restrict__ out, int M, int d, int nqb, int items, int per_xcd, int full,
+         float* __restrict__ part) {
+  constexpr int D = 64, BKV = 64;
+  constexpr int KI = 2, VI = 2;                 // DMA instructions per wave per tile (K, V^T)
+  constexpr int STAGE = (KI + VI) * 256;        // 16-byte slots per ring stage
+  __shared__ uint4 lds[3 * STAGE];
+  __shared__ int redo;
+  uint4* const sK0 = lds;
+  uint4* const sV0 = lds + KI * 256;
+  uint4* const sK1 = lds + STAGE;
+  uint4* const sV1 = lds + STAGE + KI * 256;
+  uint4* const sK2 = lds + 2 * STAGE;
+  uint4* const sV2 = lds + 2 * STAGE + KI * 256;
+
+  const int xcd = blockIdx.x & 7, u = blockIdx.x >> 3;
+  const int ibeg = xcd * per_xcd, iend = min(items, ibeg + per_xcd);
+  const int nfull = min(full, iend - ibeg);
+  int w, half = -1;
+  if (u < nfull) {
+    w = ibeg + u;
+  } else {
+    w = ibeg + nfull + ((u - nfull) >> 1);
+    half = (u - nfull) & 1;
+  }
+  if (w >= iend) return;
+  const int ntile = (M + BKV - 1) / BKV;
+  const int tb = half == 1 ? ntile / 2 : 0;     // key tiles [tb, te)
+  const int te = half == 0 ? ntile / 2 : ntile;
+  const int head = w / nqb;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c16 = lane & 15, g4 = lane >> 4;
+  const int q0 = (w - head * nqb) * 128 + wave * 32;
+  const int ldq = 2 * d;
+  const uint16_t* Qb = qk + head * D;
+  const uint16_t* Kb = qk + d + head * D;
+  const uint16_t* Vb = vt + size_t(head) * D * ldv;
+  if (tid == 0) redo = 0;
+
+  // query fragments: lane holds Q[q0 + 16 qb + c16][32 kk + 8 g4 .. + 8]
+  bf16x8 qf[2][2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int q = q0 + 16 * qb + c16;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (q < M) v = *reinterpret_cast<const uint4*>(Qb + size_t(q) * ldq + 32 * kk + 8 * g4);
+      qf[qb][kk] = __builtin_bit_cast(bf16x8, v);
+    }
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+
+  uint32_t offK[KI], offV[VI];
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const int slot = (wave * KI + i) * 64 + lane;
+    const int r = slot >> 3, c = (slot & 7) ^ swz_k16(slot >> 3);
+    offK[i] = 2u * uint32_t(r * ldq + 8 * c);
+  }
+#pragma unroll
+  for (int i = 0; i < VI; ++i) {
+    const int slot = (wave * VI + i) * 64 + lane;
+    const int r = slot >> 3, c = (slot & 7) ^ swz_v(slot >> 3);
+    offV[i] = 2u * uint32_t(r * ldv + 8 * c);
+  }
+  auto issue = [&](uint4* sk, uint4* sv, int t) {
+    const uint16_t* kt = Kb + size_t(t) * BKV * ldq;
+    const uint16_t* vtt = Vb + t * BKV;
+#pragma unroll
+    for (int i = 0; i < KI; ++i) dma16(kt, offK[i], sk + (wave * KI + i) * 64);
+#pragma unroll
+    for (int i = 0; i < VI; ++i) dma16(vtt, offV[i], sv + (wave * VI + i) * 64);
+  };
+
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
+
+  f32x4 o[4][2], lacc[2], mneg[2];
+  float mrow[2];
+  bool fail = false;
+
+  // one pass over the key tiles; safe: take the tile maximum on every tile
+  auto run = [&](bool safe) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      mrow[qb] = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { lacc[qb][i] = 0.f; mneg[qb][i] = 0.f; }
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[db][qb][i] = 0.f;
+    }
+    fail = false;
+
+    auto rescale = [&](int qb, float up) {      // m += up; O, l *= 2^-up
+      const float a = __builtin_amdgcn_exp2f(-up);
+      mrow[qb] += up;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { lacc[qb][i] *= a; mneg[qb][i] = -mrow[qb]; }
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[db][qb][i] *= a;
+    };
+
+    // scores of key block kb (16 keys) for both query blocks, with C = -m; with
+    // kMask the keys past M are set to -inf (the last tile only, so the common path
+    // is one branch-free block the scheduler can interleave)
+    auto scores = [&](const uint4* sk, int t, int kb, f32x4 (&sc)[2], auto kMask) {
+      const int row = perm16(16 * kb + c16);
+      const bf16x8 k0 = __builtin_bit_cast(bf16x8, sk[row * 8 + ((0 + g4) ^ swz_k16(row))]);
+      const bf16x8 k1 = __builtin_bit_cast(bf16x8, sk[row * 8 + ((4 + g4) ^ swz_k16(row))]);
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        sc[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf[qb][0], mneg[qb], 0, 0, 0);
+        sc[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf[qb][1], sc[qb], 0, 0, 0);
+      }
+      if constexpr (decltype(kMask)::value) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (t * BKV + perm16(16 * kb + 4 * g4 + i) >= M) {
+            sc[0][i] = -INFINITY;
+            sc[1][i] = -INFINITY;
+          }
+      }
+    };
+
+    // all scores of the tile, then per 32-key chunk: P = 2^(s - m) (bf16), O^T += V^T P^T,
+    // l += 1 P^T.  P of chunk c: keys 32 c + 8 g4 .. + 7 (blocks 2c and 2c+1, permuted rows)
+    auto body = [&](const uint4* sk, const uint4* sv, int t, auto kMask) {
+      f32x4 sb[4][2];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) scores(sk, t, kb, sb[kb], kMask);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        bf16x8 pf[2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pf[qb][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(sb[2 * c][qb][e]));
+            pf[qb][4 + e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(sb[2 * c + 1][qb][e]));
+          }
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+          const int row = 16 * db + c16;
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, sv[row * 8 + ((4 * c + g4) ^ swz_v(row))]);
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[db][qb], 0, 0, 0);
+        }
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+          lacc[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[qb], lacc[qb], 0, 0, 0);
+      }
+    };
+
+    // one tile: the tile maximum (first tile, safe pass), P V and l, then the raise check
+    auto tile = [&](const uint4* sk, const uint4* sv, int t, auto kMask, bool domax) {
+      if (domax) {
+        // the tile maximum (a separate pass over the scores, which are recomputed below)
+        float mx[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          f32x4 sc[2];
+          scores(sk, t, kb, sc, kMask);
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx[qb] = fmaxf(mx[qb], sc[qb][i]);
+        }
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          float m = fmaxf(mx[qb], __shfl_xor(mx[qb], 16, 64));
+          m = fmaxf(m, __shfl_xor(m, 32, 64));
+          const float up = t == tb ? m : fmaxf(m, 0.f);
+          if (up != 0.f) rescale(qb, up);
+        }
+      }
+      body(sk, sv, t, kMask);
+      // m lags the scores by more than about 58 (l >= 2^64, all rows of lacc hold l, or
+      // l not finite): the item is redone in the safe pass.  While l < 2^64, every P
+      // and so O stay far inside the fp32 range.
+      if (!safe) {
+        const bool big = !(lacc[0][0] < 0x1p64f && lacc[1][0] < 0x1p64f);
+        // a real branch (not a select): it ends the tile's scheduling region, which keeps
+        // the compiler from interleaving tiles (that spills; 144 VGPRs this way)
+        if (__builtin_amdgcn_ballot_w64(big) != 0) {
+          fail = true;
+          __builtin_amdgcn_s_sleep(0);
+        }
+      }
+    };
+    // tile t has landed in every wave's view; stage (nk, nv) is free for tile t + 2
+    auto sync = [&](int t, uint4* nk, uint4* nv) {
+      if (t + 1 < te) __builtin_amdgcn_s_waitcnt(0x0F70 | (KI + VI));
+      else __builtin_amdgcn_s_waitcnt(0x0F70);
+      __builtin_amdgcn_s_barrier();
+      if (t + 2 < te) issue(nk, nv, t + 2);
+    };
+    constexpr std::false_type kFull{};
+    constexpr std::true_type kPart{};
+    // tile t sits in ring stage (t - tb) % 3.  The first tile and a partial last tile
+    // run outside the loop, so the loop body is one branch-free instance per stage.
+    const bool part_last = te * BKV > M;
+    const int tm = part_last ? te - 1 : te;     // tiles [tb, tm) are full
+    issue(sK0, sV0, tb);
+    if (tb + 1 < te) issue(sK1, sV1, tb + 1);
+    sync(tb, sK2, sV2);
+    if (tb < tm) tile(sK0, sV0, tb, kFull, true);
+    else tile(sK0, sV0, tb, kPart, true);
+    for (int t = tb + 1; t < tm; t += 3) {
+      sync(t, sK0, sV0);
+      tile(sK1, sV1, t, kFull, safe);
+      if (t + 1 >= tm) break;
+      sync(t + 1, sK1, sV1);
+      tile(sK2, sV2, t + 1, kFull, safe);
+      if (t + 2 >= tm) break;
+      sync(t + 2, sK2, sV2);
+      tile(sK0, sV0, t + 2, kFull, safe);
+    }
+    if (part_last && te - 1 > tb) {
+      const int t = te - 1, q = (t - tb) % 3;
+      sync(t, sK0, sV0);                        // no further tile to prefetch
+      tile(sK0 + q * STAGE, sV0 + q * STAGE, t, kPart, safe);   // one instance, stage by address
+    }
+  };
+
+  // pass 0 is the fast path; pass 1 (rare) redoes the item with the tile maximum on
+  // every tile when any wave saw a non-finite row sum (one call site: one inlined copy)
+  for (int pass = 0;; ++pass) {
+    run(pass > 0);
+    if (pass > 0) break;
+    if (__builtin_amdgcn_ballot_w64(fail) != 0 && lane == 0) redo = 1;
+    __syncthreads();
+    if (!redo) break;
+    __syncthreads();
+  }
+
+  if (half >= 0) {
+    const int si = xcd * (per_xcd - full) + (w - ibeg - nfull);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      float* rec = part + (size_t(si) * 2 + half) * 128 * (D + 4) + size_t(wave * 32 + 16 * qb + c16) * (D + 4);
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+        *reinterpret_cast<float4*>(rec + 16 * db + 4 * g4) =
+            make_float4(o[db][qb][0], o[db][qb][1], o[db][qb][2], o[db][qb][3]);
+      if (g4 == 0) {
+        rec[D] = mrow[qb];
+        rec[D + 1] = lacc[qb][0];
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int q = q0 + 16 * qb + c16;
+    if (q >= M) continue;
+    const float inv = 1.0f / lacc[qb][0];
+    uint16_t* orow = out + size_t(q) * d + head * D;
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      ushort4 v;
+      v.x = to_bf16(o[db][qb][0] * inv);
+      v.y = to_bf16(o[db][qb][1] * inv);
+      v.z = to_bf16(o[db][qb][2] * inv);
+      v.w = to_bf16(o[db][qb][3] * inv);
+      *reinterpret_cast<ushort4*>(orow + 16 * db + 4 * g4) = v;
+    }
+  }
+}
+
 // Zero the padding columns [M, ldv) of the transposed values (never written by
 // the QKV GEMM; the attention DMA reads them and multiplies them by zero).
 __global__ void k_zero_vt_tail(uint16_t* vt, int rows, int ldv, int M) {
@@ -452,12 +763,28 @@ static int attn_slots_per_xcd() {
   return cache[dev];
 }
 
-template <int D>
+constexpr int kAttn16MinTokens = 8192;
+
+static int attn16_slots_per_xcd() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cache[dev] == 0) {
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_attn16, 256, 0) != hipSuccess)
+      return 0;
+    cache[dev] = (cus / 8) * per_cu;
+  }
+  return cache[dev];
+}
+
+template <int D, bool V16>
 static Status launch_attn(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t* out, const Geo& g,
                           int M, float* part, size_t part_bytes, hipStream_t s) {
   const int nqb = (M + 127) / 128, items = nqb * g.H, per_xcd = (items + 7) / 8;
   // split the items of the last partial round when their halves fit in one round
-  const int slots = attn_slots_per_xcd<D>();
+  const int slots = V16 ? attn16_slots_per_xcd() : attn_slots_per_xcd<D>();
   int full = per_xcd;
   if (slots > 0 && (M + 63) / 64 >= 2) {
     const int f = per_xcd / slots * slots, r = per_xcd - f;
@@ -465,8 +792,12 @@ static Status launch_attn(const uint16_t* qk, const uint16_t* vt, int ldv, uint1
     if (r > 0 && 2 * r <= slots && part && need <= part_bytes) full = f;
   }
   const int units = full + 2 * (per_xcd - full);
-  hipLaunchKernelGGL(k_attn_bf16<D>, dim3(8 * units), dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb,
-                     items, per_xcd, full, part);
+  if constexpr (V16)
+    hipLaunchKernelGGL(k_attn16, dim3(8 * units), dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb, items,
+                       per_xcd, full, part);
+  else
+    hipLaunchKernelGGL(k_attn_bf16<D>, dim3(8 * units), dim3(256), 0, s, qk, vt, ldv, out, M, g.d, nqb,
+                       items, per_xcd, full, part);
   DC_HIP(hipGetLastError());
   if (full < per_xcd) {
     hipLaunchKernelGGL(k_attn_combine<D>, dim3(8 * (per_xcd - full)), dim3(256), 0, s, part, out, M, g.d,
@@ -484,8 +815,12 @@ Status attention_bf16(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t*
     hipLaunchKernelGGL(k_zero_vt_tail, dim3(64), dim3(256), 0, s, v, g.d, ldv, M);
     DC_HIP(hipGetLastError());
   }
-  if (g.Dh == 64) return launch_attn<64>(qk, vt, ldv, out, g, M, part, part_bytes, s);
-  if (g.Dh == 72) return launch_attn<72>(qk, vt, ldv, out, g, M, part, part_bytes, s);
+  // head_dim 64: the 16x16x32 kernel from 8,192 tokens (MI355X, 17,776 x 30 heads: 1.96 vs
+  // 2.08 ms); below that its per-item first-tile pass costs more than it saves (3,597 x 30:
+  // 121 vs 119 us)
+  if (g.Dh == 64 && M >= kAttn16MinTokens) return launch_attn<64, true>(qk, vt, ldv, out, g, M, part, part_bytes, s);
+  if (g.Dh == 64) return launch_attn<64, false>(qk, vt, ldv, out, g, M, part, part_bytes, s);
+  if (g.Dh == 72) return launch_attn<72, false>(qk, vt, ldv, out, g, M, part, part_bytes, s);
   return Status::shape("bf16 attention supports head_dim 64 and 72");
 }
 

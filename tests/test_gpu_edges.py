@@ -155,3 +155,75 @@ def test_empty_index_lists_leave_buffers_untouched(api, dev):
     torch.cuda.synchronize()
     assert (h == 3.0).all() and (x == 5.0).all() and (r.float() == 2.0).all()
     assert (g == 4.0).all() and (sums == 6.0).all()
+
+
+class _AttentionOnly:
+    """Block 0 of W reduced to its attention: query rows of W_qkv multiplied by a power of
+    two (exact in bf16), W_o = I and b_o = 0, so with gate1 = 1 and gate2 = 0 the block
+    adds the attention output itself to h."""
+
+    def __init__(self, W, factor):
+        self.W, self.f = W, factor
+        self.m = W.m
+
+    def get(self, name):
+        return self.W.get(name)
+
+    def block(self, l, name):
+        d = self.m.hidden
+        if name == "w_o":
+            return np.eye(d, dtype=np.float32)
+        if name == "b_o":
+            return np.zeros(d, np.float32)
+        a = self.W.block(l, name)
+        if name == "w_qkv":
+            a = a.copy()
+            a[:d] *= self.f
+        return a
+
+
+def test_attention_large_logits(api, dev):
+    """8,269 tokens x 30 heads of 64 run the long-sequence attention kernel.  Query
+    weights scaled by 64 spread the logits of a row over hundreds of log2 units: a
+    later key tile lies far above the first tile's maximum, so the fast pass raises
+    its running maximum or, past the fp32 range, the workgroup redoes the item with
+    the tile maximum on every tile.  The block is reduced to its attention (W_o = I,
+    gate1 = 1, gate2 = 0).  The logits are so steep that rounding q and k to bf16
+    decides which key dominates, so the reference takes a, q, k and v rounded to
+    bf16 at the points where the device rounds them (q after its log2(e)/sqrt(d_h)
+    scale), then the oracle's attention; sampled rows."""
+    import math
+    import torch
+    m = _shape(1920, 30, 64, 7680, (16, 32, 64), 77, "bf16")
+    assert m.n_tok >= 8192
+    d = m.hidden
+    W = _AttentionOnly(I.Weights(m, 97), 64.0)
+    dm = api.DeviceModel(W, dev)
+    ws = api.Workspace(m, 1, dev)
+    h = I.hidden_state(m, (42,))
+    mod = mod_input(m, (43,))
+    mod[2] = 1.0                          # gate1
+    mod[5] = 0.0                          # gate2: no MLP
+    dh = t(h[None], dev)
+    say("large-logit attention N =", m.n_tok)
+    api.dc_block_forward(dm, 0, t(mod, dev), dh, [0], ws)
+    torch.cuda.synchronize()
+    got = dh[0].cpu().numpy().astype(np.float64) - h
+    assert np.isfinite(got).all()
+    rng = np.random.default_rng(1)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, m.n_v - 1, m.n_v, m.n_tok - 1],
+                                     rng.integers(0, m.n_tok, 40)]))
+    m64 = mod.astype(np.float64)
+    a = I.round_bf16(dit.modulate(h.astype(np.float64), m64[0], m64[1], 1e-6).astype(np.float32))
+    wqkv = W.block(0, "w_qkv").astype(np.float64)
+    bqkv = W.block(0, "b_qkv").astype(np.float64)
+    qkv = a.astype(np.float64) @ wqkv.T + bqkv
+    qs = np.float32(1.4426950408889634 / math.sqrt(m.head_dim))
+    q = I.round_bf16((qkv[rows, :d].astype(np.float32) * qs)).astype(np.float64)
+    k = I.round_bf16(qkv[:, d: 2 * d].astype(np.float32)).astype(np.float64)
+    v = I.round_bf16(qkv[:, 2 * d:].astype(np.float32)).astype(np.float64)
+    # q k^T is in log2 units: scale q so the oracle's softmax(q k^T / sqrt(d_h)) is base 2
+    want = dit.attention(q * (math.sqrt(m.head_dim) * math.log(2.0)), k, v, m.heads)
+    err = rel_l2(got[rows], want)
+    say("large-logit attention rel-L2", err)
+    assert err < 1e-2
