@@ -1,7 +1,9 @@
 // GEMMs of the denoising step: C = A W^T with fused epilogues.
 //
 // bf16 block GEMMs (QKV, out-projection, MLP up / down): v_mfma_f32_32x32x16_bf16,
-// 8 waves, block tile 256 x 192 x 64, tiles fed global -> LDS by LDS-DMA into two
+// 8 waves, block tile 384 x 192 x 64 (QKV, out-projection, MLP down: fewer operand
+// lines per FLOP, the L1 miss queue being the limit) or 256 x 192 x 64 (MLP up, whose
+// 40 column tiles quantise better), tiles fed global -> LDS by LDS-DMA into two
 // stages (the refill of the next k-step interleaved with this k-step's MFMAs),
 // XOR-swizzled 128-byte rows, one barrier per k-step, XCD-aware tile order;
 // epilogues take one accumulator column at a time.
@@ -684,7 +686,7 @@ Status gemm_f32_qkv(const float* A, const float* W, const float* bias, float* qk
 
 Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, uint16_t* qk,
                      uint16_t* vt, int ldv, const Geo& g, int M, hipStream_t s) {
-  return launch_dma<256, 192, 4, 2, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
+  return launch_dma<384, 192, 4, 2, 2>(A, g.d, W, g.d, M, 3 * g.d, g.d,
                                     EpiQKVBf16{bias, qk, vt, g.d, ldv,
                                                float(1.4426950408889634 / std::sqrt(double(g.Dh)))},
                                     s);
@@ -693,7 +695,7 @@ Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, ui
 Status gemm_bf16_gate_residual(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
                                const float* gate, float* h, int ldh, int M, int N, int K,
                                hipStream_t s) {
-  return launch_dma<256, 192, 4, 2, 2>(A, lda, W, K, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
+  return launch_dma<384, 192, 4, 2, 2>(A, lda, W, K, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
 }
 
 Status gemm_bf16_gelu(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
