@@ -207,6 +207,26 @@ dc_status dc_schedule_dp(const dc_sched_problem* p, dc_schedule* out);
  * share K. */
 dc_status dc_select_tau(const dc_sched_problem* problems, int32_t n, double rho, int64_t* tau_q);
 
+/* Eq. 2 for one planned pose sequence: L = sum of ||p_t - p_{t-1}||_2 and Theta = sum of
+ * |wrap(psi_t - psi_{t-1})| (wrap to [-pi, pi)), one IEEE double operation at a time (the
+ * values dc_schedule_dp reports).  pose_xy: host f64 [n_pose, 2]; pose_yaw: host f64
+ * [n_pose]; L, Theta: host out.  n_pose < 2 gives 0, 0.  Errors: DC_ERR_ARG on NULL. */
+dc_status dc_motion_statistics(const double* pose_xy, const double* pose_yaw, int32_t n_pose,
+                               double* L, double* Theta);
+
+/* Anchor selection of Sec. 3.1 over n calibration clips with motion statistics L[i],
+ * Theta[i] (host f64 [n], e.g. from dc_motion_statistics).  Both are standardised with the
+ * set's mean and population standard deviation (max(sd, eps) as the denominator).  The
+ * low-motion anchor minimises z^L + z^Theta.  Among clips whose Theta is above the set's
+ * median (mean of the two middle values for even n) and whose L and Theta are above the
+ * low-motion anchor's, the moving-turn anchor maximises z^L z^Theta.  Ties keep the lower
+ * clip index.  Out: anchors [4] = (L0, Theta0, L1, Theta1) for dc_sched_problem, index [2]
+ * = the two clip indices.  No qualifying clip: index[1] = -1, (L1, Theta1) = (L0, Theta0),
+ * DC_OK; the paper then falls back to full inference (the caller's decision).
+ * Errors: DC_ERR_ARG for n < 1, eps <= 0, non-finite statistics or NULL pointers. */
+dc_status dc_select_anchors(const double* L, const double* Theta, int32_t n, double eps,
+                            double* anchors, int32_t* index);
+
 /* ---------------------------------------------------------------------------
  * Sampler: the causal controller of Sec. 3.2 around the device steps.
  * ------------------------------------------------------------------------- */

@@ -77,6 +77,10 @@ SIGNATURES = {
                                   C.c_int32, vp, C.c_size_t, vp]),
     "dc_schedule_dp": (C.c_int32, [P(SchedProblem), P(Schedule)]),
     "dc_select_tau": (C.c_int32, [P(SchedProblem), C.c_int32, C.c_double, P(C.c_int64)]),
+    "dc_motion_statistics": (C.c_int32, [P(C.c_double), P(C.c_double), C.c_int32, P(C.c_double),
+                                         P(C.c_double)]),
+    "dc_select_anchors": (C.c_int32, [P(C.c_double), P(C.c_double), C.c_int32, C.c_double,
+                                      P(C.c_double), P(C.c_int32)]),
     "dc_sampler_create": (C.c_int32, [P(ModelCfg), P(ModelWeights), C.c_int32, P(SchedProblem),
                                       P(C.c_double), P(Buffers), C.c_int32, vp, P(vp)]),
     "dc_denoise_step": (C.c_int32, [vp, C.c_int32, vp, P(C.c_uint8), P(C.c_double)]),

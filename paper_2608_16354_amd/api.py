@@ -15,7 +15,8 @@ from .inputs import ModelShape, SchedProblem as PySchedProblem
 
 __all__ = ["model_cfg", "DeviceModel", "Workspace", "SamplerBuffers", "profile", "dc_workspace_bytes", "dc_time_modulation",
            "dc_patch_embed", "dc_block_forward", "dc_cache_store", "dc_cache_apply",
-           "dc_drift_l1", "dc_head_euler", "dc_schedule_dp", "dc_select_tau", "Sampler"]
+           "dc_drift_l1", "dc_head_euler", "dc_schedule_dp", "dc_select_tau", "dc_motion_statistics",
+           "dc_select_anchors", "Sampler"]
 
 
 def _torch():
@@ -201,6 +202,31 @@ def dc_select_tau(problems, rho: float) -> int:
     tau = C.c_int64(0)
     L.check("dc_select_tau", L.load().dc_select_tau(arr, len(cps), float(rho), C.byref(tau)))
     return int(tau.value)
+
+
+def dc_motion_statistics(xy, yaw):
+    """Eq. 2 for one pose sequence: (L, Theta)."""
+    xy = np.ascontiguousarray(xy, np.float64).reshape(-1, 2)
+    yaw = np.ascontiguousarray(yaw, np.float64)
+    n = len(yaw)
+    Lv, Tv = C.c_double(0.0), C.c_double(0.0)
+    dp = C.POINTER(C.c_double)
+    L.check("dc_motion_statistics", L.load().dc_motion_statistics(
+        xy.ctypes.data_as(dp), yaw.ctypes.data_as(dp), n, C.byref(Lv), C.byref(Tv)))
+    return float(Lv.value), float(Tv.value)
+
+
+def dc_select_anchors(Ls, Ths, eps: float):
+    """Sec. 3.1 anchors from calibration clips: ((L0, Th0, L1, Th1), (i0, i1)); i1 = None
+    when no clip qualifies (full-inference fallback)."""
+    Ls = np.ascontiguousarray(Ls, np.float64)
+    Ths = np.ascontiguousarray(Ths, np.float64)
+    out = (C.c_double * 4)()
+    idx = (C.c_int32 * 2)()
+    dp = C.POINTER(C.c_double)
+    L.check("dc_select_anchors", L.load().dc_select_anchors(
+        Ls.ctypes.data_as(dp), Ths.ctypes.data_as(dp), len(Ls), float(eps), out, idx))
+    return tuple(float(v) for v in out), (int(idx[0]), None if idx[1] < 0 else int(idx[1]))
 
 
 class SamplerBuffers:

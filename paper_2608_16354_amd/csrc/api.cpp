@@ -382,6 +382,33 @@ dc_status dc_schedule_dp(const dc_sched_problem* p, dc_schedule* out) {
   })());
 }
 
+dc_status dc_motion_statistics(const double* pose_xy, const double* pose_yaw, int32_t n_pose,
+                               double* L, double* Theta) {
+  DC_ENTRY(([&]() -> Status {
+    if (!L || !Theta || (n_pose > 0 && (!pose_xy || !pose_yaw))) return Status::arg("NULL argument");
+    if (n_pose < 0) return Status::arg("n_pose must be >= 0");
+    motion_statistics(pose_xy, pose_yaw, n_pose, *L, *Theta);
+    return Status::ok();
+  })());
+}
+
+dc_status dc_select_anchors(const double* L, const double* Theta, int32_t n, double eps, double* anchors,
+                            int32_t* index) {
+  DC_ENTRY(([&]() -> Status {
+    if (!L || !Theta || !anchors || !index) return Status::arg("NULL argument");
+    if (!(eps > 0.0)) return Status::arg("eps must be positive");
+    int i0 = 0, i1 = -1;
+    DC_TRY(select_anchors(L, Theta, n, eps, i0, i1));
+    index[0] = i0;
+    index[1] = i1;
+    anchors[0] = L[i0];
+    anchors[1] = Theta[i0];
+    anchors[2] = i1 >= 0 ? L[i1] : L[i0];
+    anchors[3] = i1 >= 0 ? Theta[i1] : Theta[i0];
+    return Status::ok();
+  })());
+}
+
 dc_status dc_select_tau(const dc_sched_problem* problems, int32_t n, double rho, int64_t* tau_q) {
   DC_ENTRY(([&]() -> Status {
     if (!problems || !tau_q) return Status::arg("NULL argument");

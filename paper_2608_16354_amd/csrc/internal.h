@@ -53,6 +53,8 @@ Status scene_tables(const dc_sched_problem& p, SceneTables& t);
 Status schedule(const dc_sched_problem& p, const SceneTables& t, std::vector<uint8_t>& reuse,
                 int32_t& n_reuse, int64_t& cost_q);
 Status select_tau(const dc_sched_problem* probs, int n, double rho, int64_t& tau);
+void motion_statistics(const double* xy, const double* yaw, int n_pose, double& L, double& Th);
+Status select_anchors(const double* L, const double* Th, int n, double eps, int& i0, int& i1);
 
 // ---------------------------------------------------------------------------
 // model geometry

@@ -28,17 +28,23 @@ static double wrap_angle(double a) {
   return a - two_pi * turns;
 }
 
-Status scene_tables(const dc_sched_problem& p, SceneTables& t) {
-  const int K = p.K, H = p.h_max;
-  // Eq. 2: path length and accumulated absolute heading change.
-  double L = 0.0, Th = 0.0;
-  for (int i = 1; i < p.n_pose; ++i) {
-    const double dx = p.pose_xy[2 * i] - p.pose_xy[2 * (i - 1)];
-    const double dy = p.pose_xy[2 * i + 1] - p.pose_xy[2 * (i - 1) + 1];
+// Eq. 2: path length and accumulated absolute heading change of a planned pose sequence.
+void motion_statistics(const double* xy, const double* yaw, int n_pose, double& L, double& Th) {
+  L = 0.0;
+  Th = 0.0;
+  for (int i = 1; i < n_pose; ++i) {
+    const double dx = xy[2 * i] - xy[2 * (i - 1)];
+    const double dy = xy[2 * i + 1] - xy[2 * (i - 1) + 1];
     const double sq = dx * dx + dy * dy;
     L = L + std::sqrt(sq);
-    Th = Th + std::fabs(wrap_angle(p.pose_yaw[i] - p.pose_yaw[i - 1]));
+    Th = Th + std::fabs(wrap_angle(yaw[i] - yaw[i - 1]));
   }
+}
+
+Status scene_tables(const dc_sched_problem& p, SceneTables& t) {
+  const int K = p.K, H = p.h_max;
+  double L = 0.0, Th = 0.0;
+  motion_statistics(p.pose_xy, p.pose_yaw, p.n_pose, L, Th);
   // Eq. 3: position relative to the two anchors; Eq. 4: one interpolation coordinate.
   const double zL = (L - p.L0) / std::max(p.L1 - p.L0, p.eps);
   const double zTh = (Th - p.Th0) / std::max(p.Th1 - p.Th0, p.eps);
@@ -171,6 +177,51 @@ Status validate_problem(const dc_sched_problem& p) {
   if (!p.legal) return Status::arg("legal mask missing");
   if (p.K > 1 && (!p.q0 || !p.q1 || !p.d0 || !p.d1)) return Status::arg("response/drift tables missing");
   if (!(p.eps >= 0.0)) return Status::arg("eps must be >= 0");
+  return Status::ok();
+}
+
+// Sec. 3.1 anchor selection.  z-scores use the calibration set's mean and population
+// standard deviation (a zero deviation is replaced by eps); the low-motion anchor has the
+// smallest z^L + z^Theta; the moving-turn anchor, among clips with Theta above the
+// calibration median (the mean of the two middle values for an even count) and L, Theta
+// above the low-motion anchor's, has the largest z^L z^Theta; ties keep the lower index.
+static void standardise(const double* x, int n, double eps, std::vector<double>& z) {
+  double s = 0.0;
+  for (int i = 0; i < n; ++i) s = s + x[i];
+  const double mean = s / n;
+  double ss = 0.0;
+  for (int i = 0; i < n; ++i) {
+    const double dv = x[i] - mean;
+    ss = ss + dv * dv;
+  }
+  const double den = std::max(std::sqrt(ss / n), eps);
+  z.resize(n);
+  for (int i = 0; i < n; ++i) z[i] = (x[i] - mean) / den;
+}
+
+Status select_anchors(const double* L, const double* Th, int n, double eps, int& i0, int& i1) {
+  if (n < 1) return Status::arg("need at least one calibration clip");
+  for (int i = 0; i < n; ++i)
+    if (!std::isfinite(L[i]) || !std::isfinite(Th[i])) return Status::arg("motion statistics must be finite");
+  std::vector<double> zL, zT;
+  standardise(L, n, eps, zL);
+  standardise(Th, n, eps, zT);
+  i0 = 0;
+  double best = zL[0] + zT[0];
+  for (int i = 1; i < n; ++i) {
+    const double v = zL[i] + zT[i];
+    if (v < best) { i0 = i; best = v; }
+  }
+  std::vector<double> srt(Th, Th + n);
+  std::sort(srt.begin(), srt.end());
+  const double med = (n % 2 == 1) ? srt[n / 2] : (srt[n / 2 - 1] + srt[n / 2]) / 2.0;
+  i1 = -1;
+  double best1 = 0.0;
+  for (int i = 0; i < n; ++i) {
+    if (!(Th[i] > med && L[i] > L[i0] && Th[i] > Th[i0])) continue;
+    const double v = zL[i] * zT[i];
+    if (i1 < 0 || v > best1) { i1 = i; best1 = v; }
+  }
   return Status::ok();
 }
 

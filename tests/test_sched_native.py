@@ -86,3 +86,68 @@ def test_invalid_problems_are_rejected():
         with pytest.raises(api.L.DriveCacheError) as e:
             api.dc_schedule_dp(p.replace(**bad))
         assert e.value.code == api.L.DC_ERR_ARG
+
+
+def test_motion_statistics_match_oracle_bitwise():
+    rng = np.random.default_rng(7)
+    for _ in range(300):
+        n = int(rng.integers(0, 60))
+        xy = np.cumsum(rng.normal(0.0, 2.0, (n, 2)), axis=0)
+        # headings drift past +-pi, so the wrap of Eq. 2 is exercised
+        yaw = np.cumsum(rng.normal(0.0, 1.5, n)) if n else np.zeros(0)
+        got = api.dc_motion_statistics(xy, yaw)
+        want = planner.motion_statistics(xy, yaw)
+        assert got == want
+
+
+def _random_anchor_set(rng):
+    n = int(rng.integers(1, 40))
+    if rng.random() < 0.3:        # coarse values: many ties and repeated clips
+        L = rng.integers(0, 5, n) * 7.5
+        Th = rng.integers(0, 4, n) * 0.125
+    else:
+        L = rng.uniform(0.0, 60.0, n)
+        Th = rng.uniform(0.0, 1.2, n)
+    return L.astype(np.float64), Th.astype(np.float64)
+
+
+def test_select_anchors_matches_oracle_bitwise():
+    from oracle import anchors
+    rng = np.random.default_rng(8)
+    fallbacks = 0
+    for _ in range(2000):
+        L, Th = _random_anchor_set(rng)
+        (L0, T0, L1, T1), (i0, i1) = api.dc_select_anchors(L, Th, 1e-6)
+        j0, j1 = anchors.select_anchors(L.tolist(), Th.tolist(), 1e-6)
+        assert (i0, i1) == (j0, j1)
+        assert (L0, T0) == (L[i0], Th[i0])
+        if i1 is None:
+            fallbacks += 1
+            assert (L1, T1) == (L0, T0)
+        else:
+            assert (L1, T1) == (L[i1], Th[i1])
+    assert fallbacks > 0
+
+
+def test_select_anchors_on_the_calibration_plans():
+    """Eq. 2 of the 32 seeded calibration plans (12-step horizon, 10 Hz) through the
+    library, then the anchor rule, equal to the oracle on the same plans."""
+    from oracle import anchors
+    w = I.WORKLOADS["dit-30x1920-bf16"]
+    stats = [api.dc_motion_statistics(*I.poses(m, w.n_pose, w.dt)) for m in I.calibration_motions(32)]
+    Ls = [s[0] for s in stats]
+    Ths = [s[1] for s in stats]
+    (L0, T0, L1, T1), (i0, i1) = api.dc_select_anchors(Ls, Ths, w.eps)
+    assert (i0, i1) == anchors.select_anchors(Ls, Ths, w.eps)
+    assert i1 is not None and L1 > L0 and T1 > T0
+
+
+def test_select_anchors_rejects_bad_input():
+    from paper_2608_16354_amd import _lib
+    with pytest.raises(RuntimeError):
+        api.dc_select_anchors([], [], 1e-6)
+    with pytest.raises(RuntimeError):
+        api.dc_select_anchors([1.0], [0.1], 0.0)
+    with pytest.raises(RuntimeError):
+        api.dc_select_anchors([1.0, float("nan")], [0.1, 0.2], 1e-6)
+    assert _lib.load().dc_select_anchors(None, None, 1, 1e-6, None, None) == _lib.DC_ERR_ARG
