@@ -232,6 +232,11 @@ Status head_euler(const Geo& g, const dc_model_weights* w, const float* head_mod
     const int b = il.v[i];
     const float* gb = gin + size_t(b) * g.N * g.d;
     ProfScope ps(KClass::kHead, s);
+    if (head_euler_fused_ok(g)) {
+      DC_TRY(head_euler_bf16(gb, static_cast<const uint16_t*>(w->w_head), w->b_head, head_mod,
+                             head_mod + g.d, x + size_t(b) * lat, dsigma, g, s));
+      continue;
+    }
     DC_TRY(ln_modulate(gb, g.Nv, g.d, head_mod, head_mod + g.d, at<void>(ws, L.a), g.d, g.bf16, g, s));
     if (g.bf16)
       DC_TRY(gemm_bf16_head(at<uint16_t>(ws, L.a), g.d, static_cast<const uint16_t*>(w->w_head),

@@ -7,8 +7,9 @@
 // stages (the refill of the next k-step interleaved with this k-step's MFMAs),
 // XOR-swizzled 128-byte rows, one barrier per k-step, XCD-aware tile order;
 // epilogues take one accumulator column at a time.
-// bf16 head + Euler: the same LDS-DMA GEMM with a 64 x 64 tile (N = 64 outputs)
-// and the unpatchify + Euler epilogue.
+// bf16 head + Euler for models wider than the one-pass head kernel takes (d > 2048):
+// the same LDS-DMA GEMM with a 64 x 64 tile (N = 64 outputs) and the unpatchify +
+// Euler epilogue, after LN-modulation to bf16 rows.
 // bf16 patch embedding: fp32-accurate split-bf16 MFMA with the patchify gather fused.
 // f32 path: a plain SIMT tiled kernel for the fp32 model and the small fp32
 // GEMMs (patch embedding of the fp32 model, timestep MLP).

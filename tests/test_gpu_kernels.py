@@ -208,7 +208,16 @@ class _OneBlock:
         return self.W.block(self.l, name)
 
 
-@pytest.mark.parametrize("name", SMALL + ["dit-30x1920-bf16"])
+def _head_tol(m):
+    """The bf16 head with d <= 2048 is the fused one-pass kernel, which feeds the matrix
+    cores split (hi + lo) bf16 operands and so stays near fp32 accuracy; wider bf16 models
+    take LN-modulation to bf16 rows, then the GEMM."""
+    if not _bf(m):
+        return 1e-5
+    return 1e-4 if m.hidden <= 2048 else 1e-2
+
+
+@pytest.mark.parametrize("name", ALL)
 def test_head_euler(api, dev, name):
     import torch
     w = I.WORKLOADS[name]
@@ -229,7 +238,7 @@ def test_head_euler(api, dev, name):
     want = dit.euler(x.astype(np.float64), v, 0.52, 0.5)
     err = rel_l2(got - x, want - x)
     say(name, "head update rel-L2", err)
-    assert err < (1e-2 if _bf(m) else 1e-5)
+    assert err < _head_tol(m)
 
 
 class _Head:
