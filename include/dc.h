@@ -103,7 +103,9 @@ typedef struct {
 } dc_model_weights;
 
 /* ---------------------------------------------------------------------------
- * Device steps of the hot path.  All pointers are device memory unless noted.
+ * Device steps of the hot path.  All pointers are device memory unless noted,
+ * 16-byte aligned (hipMalloc and PyTorch's allocator give 256; per-sample slices
+ * of the [B, ...] buffers keep it because hidden is a multiple of 128).
  * ------------------------------------------------------------------------- */
 
 /* Bytes of scratch device memory the calls below need for a batch of B. */

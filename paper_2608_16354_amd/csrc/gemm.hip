@@ -511,20 +511,32 @@ Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M,
 // product is hi*Whi + lo*Whi + hi*Wlo (the dropped lo*Wlo is ~2^-18 relative).
 // The patchify gather is fused: each lane reads its 8 patch-vector entries
 // straight from the latent.  A workgroup = 8 waves x 32 tokens x a 128-wide
-// column chunk; the chunk of W_pe is split once into LDS and shared.
+// column chunk; the chunk of W_pe is split once into LDS and shared.  Work items
+// (token block, column chunk) are dealt so that an XCD runs every column chunk of
+// a contiguous range of token blocks, so each XCD's L2 fetches only its own part
+// of the latent.  Each wave's 32 x 32 result tiles go through LDS, so the output
+// rows leave as 16-byte stores (8 rows x 128 bytes per instruction) and the
+// positional rows arrive as 8-byte loads.
 // ---------------------------------------------------------------------------
 struct PatchGeo { int T, Hl, Wl, p, lp, Hp, Wp; };   // lp = log2(p)
+
+constexpr int kPeStride = 40;   // floats per row of a wave's 32 x 32 result tile in LDS
 
 __global__ void __launch_bounds__(512) k_patch_embed_bf16(const float* __restrict__ x,
                                                           const float* __restrict__ W,
                                                           const float* __restrict__ bias,
                                                           const uint16_t* __restrict__ pos,
                                                           float* __restrict__ out, int Nv, int d,
-                                                          PatchGeo pg) {
+                                                          int items, int per_xcd, PatchGeo pg) {
   __shared__ uint4 wh[128 * 8], wl[128 * 8];     // [n][16-byte chunk of k], swizzled
+  __shared__ __attribute__((aligned(16))) float res[8][32 * kPeStride];
+  const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (item >= items) return;
+  const int ncc = d >> 7;
+  const int tb = item / ncc, cc = item - tb * ncc;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r32 = lane & 31, hi = lane >> 5;
-  const int n0 = blockIdx.y * 128;
+  const int n0 = cc * 128;
   // stage W[n0 .. n0 + 128)[0 .. 64) as bf16 hi / lo: thread -> (row, 4 chunks of 4 k)
   {
     const int n = tid >> 2, k4 = (tid & 3) * 16;    // 16 consecutive k per thread
@@ -549,8 +561,22 @@ __global__ void __launch_bounds__(512) k_patch_embed_bf16(const float* __restric
           make_uint2(l[0] | (uint32_t(l[1]) << 16), l[2] | (uint32_t(l[3]) << 16));
     }
   }
+  const int m0 = tb * 256 + wave * 32;
+  // epilogue role of a lane: rows 8 q + lane / 8 (q < 4) of a 32 x 32 tile, columns
+  // 4 (lane % 8) ..; the positional rows of the next tile are loaded one tile ahead
+  // (rows clamped into the table)
+  const int er = lane >> 3, ec = 4 * (lane & 7);
+  auto load_pos = [&](int tile, uint2 (&pv)[4], float4& b4) {
+    const int nc = n0 + 32 * tile + ec;
+    b4 = *reinterpret_cast<const float4*>(bias + nc);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      pv[q] = *reinterpret_cast<const uint2*>(pos + size_t(min(m0 + 8 * q + er, Nv - 1)) * d + nc);
+  };
+  uint2 pv[4];
+  float4 b4;
+  load_pos(0, pv, b4);
   // A fragments: token m, patch-vector entries 16 kk + 8 hi + e
-  const int m0 = blockIdx.x * 256 + wave * 32;
   const int m = min(m0 + r32, Nv - 1);
   const int t = m / (pg.Hp * pg.Wp), i = (m / pg.Wp) % pg.Hp, j = m % pg.Wp;
   bf16x8 ah[4], al[4];
@@ -566,6 +592,7 @@ __global__ void __launch_bounds__(512) k_patch_embed_bf16(const float* __restric
       al[kk][e] = static_cast<__bf16>(v - static_cast<float>(h));
     }
   __syncthreads();
+  float* const rt = res[wave];
 #pragma unroll
   for (int tile = 0; tile < 4; ++tile) {
     f32x16 acc;
@@ -581,22 +608,28 @@ __global__ void __launch_bounds__(512) k_patch_embed_bf16(const float* __restric
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[kk], bh, acc, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[kk], bl, acc, 0, 0, 0);
     }
-    const int n = n0 + nr;
-    const float bn = bias[n];
-    float pv[16];
+    const int nc = n0 + 32 * tile + ec;             // this lane's 4 output columns
+    uint2 pn[4];
+    float4 bn = b4;
+    if (tile < 3) load_pos(tile + 1, pn, bn);
+    // accumulator element r of lane (r32, hi): row 8 (r / 4) + 4 hi + r % 4, column r32
 #pragma unroll
-    for (int r = 0; r < 16; ++r)   // rows clamped into the table: all 16 loads issue together
-      pv[r] = from_bf16(pos[size_t(min(m0 + 8 * (r >> 2) + 4 * hi + (r & 3), Nv - 1)) * d + n]);
-    if (m0 + 32 <= Nv) {
+    for (int r = 0; r < 16; ++r) rt[(8 * (r >> 2) + 4 * hi + (r & 3)) * kPeStride + r32] = acc[r];
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        out[size_t(m0 + 8 * (r >> 2) + 4 * hi + (r & 3)) * d + n] = (acc[r] + bn) + pv[r];
-    } else {
+    for (int q = 0; q < 4; ++q) {
+      const int mm = m0 + 8 * q + er;
+      const float4 a = *reinterpret_cast<const float4*>(rt + (8 * q + er) * kPeStride + ec);
+      float4 o;
+      o.x = (a.x + b4.x) + __uint_as_float(pv[q].x << 16);
+      o.y = (a.y + b4.y) + __uint_as_float(pv[q].x & 0xFFFF0000u);
+      o.z = (a.z + b4.z) + __uint_as_float(pv[q].y << 16);
+      o.w = (a.w + b4.w) + __uint_as_float(pv[q].y & 0xFFFF0000u);
+      if (mm < Nv) store_nt(out + size_t(mm) * d + nc, o);
+    }
+    if (tile < 3) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int mm = m0 + 8 * (r >> 2) + 4 * hi + (r & 3);
-        if (mm < Nv) out[size_t(mm) * d + n] = (acc[r] + bn) + pv[r];
-      }
+      for (int q = 0; q < 4; ++q) pv[q] = pn[q];
+      b4 = bn;
     }
   }
 }
@@ -730,9 +763,12 @@ Status patch_embed_bf16(const float* x, const float* W, const float* bias, const
   int lp = 0;
   while ((1 << lp) < g.p) ++lp;
   if ((1 << lp) != g.p) return Status::shape("bf16 patch embedding needs a power-of-two patch");
+  if (!al16(out) || !al16(bias) || !al16(pos) || !al16(W))
+    return Status::arg("bf16 patch embedding needs 16-byte aligned device buffers");
   const PatchGeo pg{g.T, g.Hl, g.Wl, g.p, lp, g.Hp, g.Wp};
-  hipLaunchKernelGGL(k_patch_embed_bf16, dim3((g.Nv + 255) / 256, g.d / 128), dim3(512), 0, s, x, W,
-                     bias, pos, out, g.Nv, g.d, pg);
+  const int items = (g.Nv + 255) / 256 * (g.d / 128), per_xcd = (items + 7) / 8;
+  hipLaunchKernelGGL(k_patch_embed_bf16, dim3(8 * per_xcd), dim3(512), 0, s, x, W, bias, pos, out,
+                     g.Nv, g.d, items, per_xcd, pg);
   DC_HIP(hipGetLastError());
   return Status::ok();
 }
