@@ -256,6 +256,38 @@ dc_status dc_sampler_create(const dc_model_cfg* cfg, const dc_model_weights* w, 
                             const dc_buffers* buf, int32_t drift_metric, hipStream_t stream,
                             dc_sampler** out);
 
+/* Options of dc_sampler_create_ex; zero-initialise, then set what is used.
+ * Model-specific legality (Sec. 3.2, last paragraph; Table 4):
+ *  - Two experts: steps k >= k_switch run w_low (its own patch embedding,
+ *    conditioning, blocks and head) with the modulation table mod_low
+ *    (f32 [K, L+1, 6, d], filled at creation); earlier steps run the weights
+ *    passed to the create call.  No cached entry crosses the switch: every
+ *    scene's problem must change segment at k_switch (else DC_ERR_ARG).
+ *    w_low NULL: one backbone.
+ *  - Guidance branches: cfg = 1 adds to every scene an unconditional branch on
+ *    txt_null (f32 [B, N_t, d]) with its own residual cache, and x moves along
+ *    v_u + guidance (v_c - v_u).  Then h_in, h and resid of dc_buffers hold
+ *    2B entries (entry B + b is scene b's unconditional branch), ws must hold
+ *    dc_workspace_bytes(cfg, 2B) bytes and B <= 32; u_ref and sums keep B.
+ *    Both branches share every step's decision; the drift check (on the video
+ *    rows, which do not depend on the text) runs once per scene. */
+typedef struct {
+  int32_t drift_metric;                /* as in dc_sampler_create */
+  const dc_model_weights* w_low;       /* low-noise expert, or NULL */
+  int32_t k_switch;                    /* first step of w_low, in 2..K */
+  float* mod_low;                      /* [K, L+1, 6, d] modulation table of w_low */
+  int32_t cfg;                         /* 1: guidance branches */
+  float guidance;                      /* guidance scale w */
+  const float* txt_null;               /* [B, N_t, d] unconditional text */
+} dc_sampler_opts;
+
+/* dc_sampler_create with the options above (NULL opts = drift_metric 0, one
+ * backbone, no guidance). */
+dc_status dc_sampler_create_ex(const dc_model_cfg* cfg, const dc_model_weights* w, int32_t B,
+                               const dc_sched_problem* problems, const double* sigmas,
+                               const dc_buffers* buf, const dc_sampler_opts* opts,
+                               hipStream_t stream, dc_sampler** out);
+
 /* Denoising step k (1-based, called for k = 1..K in order) of every scene.
  * realized: host uint8 [B] out (1 = reused, 0 = backbone evaluated); drift: host f64
  * [B] out (observed drift, NaN where no check ran).  Waits on `stream` once if any

@@ -16,6 +16,18 @@ Per scene and step k (Sec. 3.2):
 Reading (Eq. 12 vs the workload's stated metric): the distance is selectable:
 "l1" uses sums of absolute values, "l2" the Euclidean norms of Eq. 12; both use
 the whole per-scene video-row tensor.
+
+Model-specific legality (Sec. 3.2, last paragraph; Table 4):
+  * two experts (a high-noise backbone for steps k < k_switch, a low-noise one from
+    k_switch on): each step runs the active expert's whole network (patch embedding,
+    conditioning, blocks, head); no cached entry crosses the switch, which the
+    scene's segment[] expresses (a segment change at k_switch), so step k_switch
+    always evaluates the backbone;
+  * guidance branches: a conditional branch (txt) and an unconditional one
+    (txt_null) with separate residual caches, combined as
+    v = v_u + w (v_c - v_u) before the Euler update.  Both branches share the
+    step's decision; u (block 0's modulated input of the video rows) does not
+    depend on the text, so the one drift check serves both.
 """
 from __future__ import annotations
 
@@ -66,14 +78,23 @@ def drift_value(sums, eps, metric="l1"):
     return math.sqrt(s3) / (math.sqrt(s4) + eps)
 
 
-def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=()):
+def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
+           W_low=None, k_switch=None, guidance=None, txt_null=None):
     """One cached K-step sample of one scene.
 
     W: `Weights`; x1 [C,T,H,W]; txt [n_txt, d]; sigmas [K+1]; prob: `SchedProblem`.
     uncached=True runs every step in full with no drift checks (the plain sampler).
     force_veto: steps whose planned reuse is rejected regardless of the drift
-    (exercises the veto path)."""
-    P = dit.Params(W)
+    (exercises the veto path).
+    W_low, k_switch: the low-noise expert and the first step it runs (prob.segment
+    must change at k_switch).  guidance, txt_null: the guidance scale w and the
+    unconditional text; the branches keep separate caches."""
+    experts = [dit.Params(W)]
+    if W_low is not None:
+        if prob.segment is None or prob.segment[k_switch - 1] == prob.segment[k_switch - 2]:
+            raise ValueError("a two-expert scene needs a segment change at k_switch")
+        experts.append(dit.Params(W_low))
+    cfg = guidance is not None
     m = W.m
     K = prob.K
     x = x1.astype(np.float64)
@@ -86,11 +107,14 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=())
     j = 1
     age = 0
     r = None
+    r_u = None
     u_ref = None
     records = []
     for k in range(1, K + 1):
+        P = experts[1] if (W_low is not None and k >= k_switch) else experts[0]
         mods, head_mod = dit.step_modulation(P, sigmas[k - 1])
         h_in = dit.embed(P, x, txt)
+        h_in_u = dit.embed(P, x, txt_null) if cfg else None
         u = dit.backbone_input(P, h_in, mods[0])
         planned = 0 if (uncached or k == 1) else mask[k - 1]
         rec = StepRecord(k=k, planned=planned, drift=None, drift_l2=None, threshold=None,
@@ -111,10 +135,15 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=())
                 rec.vetoed = True
         if reuse:
             g = h_in[: m.n_v] + r
+            g_u = h_in_u[: m.n_v] + r_u if cfg else None
         else:
             h_out = dit.backbone(P, mods, h_in)
             r = h_out[: m.n_v] - h_in[: m.n_v]
             g = h_out[: m.n_v]
+            if cfg:
+                h_out_u = dit.backbone(P, mods, h_in_u)
+                r_u = h_out_u[: m.n_v] - h_in_u[: m.n_v]
+                g_u = h_out_u[: m.n_v]
             u_ref = u
             j, age = k, 0
             if rec.vetoed:
@@ -125,5 +154,8 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=())
         rec.j, rec.age = j, age
         records.append(rec)
         v = dit.head(P, head_mod, g)
+        if cfg:
+            v_u = dit.head(P, head_mod, g_u)
+            v = v_u + guidance * (v - v_u)
         x = dit.euler(x, v, sigmas[k - 1], sigmas[k])
     return SampleResult(x, records, plans, C, mask)

@@ -57,6 +57,11 @@ class Buffers(C.Structure):
                 ("mod", vp), ("sums", vp), ("ws", vp), ("ws_bytes", C.c_size_t)]
 
 
+class SamplerOpts(C.Structure):
+    _fields_ = [("drift_metric", C.c_int32), ("w_low", C.POINTER(ModelWeights)), ("k_switch", C.c_int32),
+                ("mod_low", vp), ("cfg", C.c_int32), ("guidance", C.c_float), ("txt_null", vp)]
+
+
 P = C.POINTER
 i32p = P(C.c_int32)
 
@@ -83,6 +88,8 @@ SIGNATURES = {
                                       P(C.c_double), P(C.c_int32)]),
     "dc_sampler_create": (C.c_int32, [P(ModelCfg), P(ModelWeights), C.c_int32, P(SchedProblem),
                                       P(C.c_double), P(Buffers), C.c_int32, vp, P(vp)]),
+    "dc_sampler_create_ex": (C.c_int32, [P(ModelCfg), P(ModelWeights), C.c_int32, P(SchedProblem),
+                                         P(C.c_double), P(Buffers), P(SamplerOpts), vp, P(vp)]),
     "dc_denoise_step": (C.c_int32, [vp, C.c_int32, vp, P(C.c_uint8), P(C.c_double)]),
     "dc_sampler_plan": (C.c_int32, [vp, C.c_int32, P(C.c_uint8), i32p, P(C.c_int64)]),
     "dc_sampler_destroy": (None, [vp]),

@@ -230,21 +230,26 @@ def dc_select_anchors(Ls, Ths, eps: float):
 
 
 class SamplerBuffers:
-    """Caller-owned device buffers for a batch of B scenes (allocated once, reusable)."""
+    """Caller-owned device buffers for a batch of B scenes (allocated once, reusable).
+    branches = 2 (guidance): h_in, h and resid hold 2B entries and the workspace 2B;
+    experts = 2: a second modulation table for the low-noise expert."""
 
-    def __init__(self, m: ModelShape, B: int, K: int, device="cuda:0"):
+    def __init__(self, m: ModelShape, B: int, K: int, device="cuda:0", branches=1, experts=1):
         torch = _torch()
         mdt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
         self.m, self.B, self.K = m, B, K
+        E = branches * B
         self.x = torch.empty((B,) + tuple(m.latent_shape), device=device, dtype=torch.float32)
         self.txt = torch.zeros((B, m.n_txt, m.hidden), device=device, dtype=torch.float32)
-        self.h_in = torch.empty((B, m.n_tok, m.hidden), device=device, dtype=torch.float32)
+        self.txt_null = torch.zeros_like(self.txt) if branches == 2 else None
+        self.h_in = torch.empty((E, m.n_tok, m.hidden), device=device, dtype=torch.float32)
         self.h = torch.empty_like(self.h_in)
-        self.resid = torch.empty((B, m.n_v, m.hidden), device=device, dtype=mdt)
-        self.u_ref = torch.empty_like(self.resid)
+        self.resid = torch.empty((E, m.n_v, m.hidden), device=device, dtype=mdt)
+        self.u_ref = torch.empty((B, m.n_v, m.hidden), device=device, dtype=mdt)
         self.mod = torch.empty((K, m.n_blocks + 1, 6, m.hidden), device=device, dtype=torch.float32)
+        self.mod_low = torch.empty_like(self.mod) if experts == 2 else None
         self.sums = torch.zeros((B, 4), device=device, dtype=torch.float64)
-        self.ws = Workspace(m, B, device)
+        self.ws = Workspace(m, E, device)
         self.c = L.Buffers(_ptr(self.x), _ptr(self.txt), _ptr(self.h_in), _ptr(self.h), _ptr(self.resid),
                            _ptr(self.u_ref), _ptr(self.mod), _ptr(self.sums), self.ws.ptr, self.ws.nbytes)
 
@@ -256,10 +261,16 @@ class Sampler:
     host or device); they are copied into `bufs` (allocated here if not given)."""
 
     def __init__(self, dm: DeviceModel, problems, sigmas, x1, txt, drift_metric=0, stream=None,
-                 bufs: SamplerBuffers = None):
+                 bufs: SamplerBuffers = None, low_expert=None, guidance=None):
+        """low_expert: (DeviceModel, k_switch), the low-noise expert from step k_switch on
+        (every problem's segment must change there); guidance: (w, txt_null [B, N_t, d]),
+        guidance branches with separate caches."""
         B = len(problems)
         self.dm, self.B, self.K = dm, B, problems[0].K
-        self.bufs = bufs if bufs is not None else SamplerBuffers(dm.m, B, self.K, dm.device)
+        if bufs is None:
+            bufs = SamplerBuffers(dm.m, B, self.K, dm.device, branches=2 if guidance else 1,
+                                  experts=2 if low_expert else 1)
+        self.bufs = bufs
         assert self.bufs.B == B and self.bufs.K == self.K
         self.bufs.x.copy_(x1, non_blocking=True)
         if dm.m.n_txt:
@@ -269,9 +280,26 @@ class Sampler:
         arr = (L.SchedProblem * B)(*[c.c for c in self._cps])
         sig = np.ascontiguousarray(np.asarray(sigmas, np.float64))
         self._h = C.c_void_p()
-        L.check("dc_sampler_create", L.load().dc_sampler_create(
+        opts = L.SamplerOpts()
+        opts.drift_metric = int(drift_metric)
+        self._low = None
+        if low_expert is not None:
+            self._low, k_switch = low_expert
+            assert self.bufs.mod_low is not None
+            opts.w_low = C.pointer(self._low.cweights)
+            opts.k_switch = int(k_switch)
+            opts.mod_low = int(self.bufs.mod_low.data_ptr())
+        if guidance is not None:
+            w, txt_null = guidance
+            assert self.bufs.txt_null is not None
+            if dm.m.n_txt:
+                self.bufs.txt_null.copy_(txt_null, non_blocking=True)
+            opts.cfg = 1
+            opts.guidance = float(w)
+            opts.txt_null = int(self.bufs.txt_null.data_ptr())
+        L.check("dc_sampler_create_ex", L.load().dc_sampler_create_ex(
             C.byref(dm.cfg), C.byref(dm.cweights), B, arr, sig.ctypes.data_as(C.POINTER(C.c_double)),
-            C.byref(self.bufs.c), int(drift_metric), _stream(stream), C.byref(self._h)))
+            C.byref(self.bufs.c), C.byref(opts), _stream(stream), C.byref(self._h)))
         self.k = 0
 
     def step(self, stream=None):

@@ -76,6 +76,14 @@ struct dc_sampler {
   dc_model_cfg cfg;
   dc_model_weights w;
   std::vector<dc_block_weights> blocks;
+  bool two = false;                  // two experts: w_low from step k_switch on
+  dc_model_weights w_low{};
+  std::vector<dc_block_weights> blocks_low;
+  int k_switch = 0;
+  float* mod_low = nullptr;
+  bool cfg_on = false;               // guidance branches (entries B..2B-1 unconditional)
+  float guidance = 1.0f;
+  const float* txt_null = nullptr;
   int B = 0, K = 0;
   std::vector<double> sigmas;
   dc_buffers buf;
@@ -93,23 +101,42 @@ namespace {
 
 Status create(const dc_model_cfg* cfg, const dc_model_weights* w, int32_t B,
               const dc_sched_problem* problems, const double* sigmas, const dc_buffers* buf,
-              int32_t metric, hipStream_t stream, dc_sampler** out) {
+              const dc_sampler_opts& o, hipStream_t stream, dc_sampler** out) {
   if (!out || !w || !problems || !sigmas || !buf) return Status::arg("NULL argument");
   *out = nullptr;
-  if (B < 1 || B > DC_MAX_BATCH) return Status::arg("B must be in [1, DC_MAX_BATCH]");
+  const int32_t metric = o.drift_metric;
+  const bool cfg_on = o.cfg != 0;
+  if (B < 1 || B > (cfg_on ? DC_MAX_BATCH / 2 : DC_MAX_BATCH))
+    return Status::arg("B must be in [1, DC_MAX_BATCH] (in [1, DC_MAX_BATCH / 2] with guidance)");
   if (metric != 0 && metric != 1) return Status::arg("drift_metric must be 0 or 1");
+  if (o.cfg != 0 && o.cfg != 1) return Status::arg("opts->cfg must be 0 or 1");
   auto s = std::make_unique<dc_sampler>();
   DC_TRY(make_geo(cfg, s->g));
   if (!buf->x || !buf->h_in || !buf->h || !buf->resid || !buf->u_ref || !buf->mod || !buf->sums ||
       !buf->ws || (s->g.Nt > 0 && !buf->txt))
     return Status::arg("a device buffer is NULL");
-  if (buf->ws_bytes < workspace_layout(s->g, B).total)
+  if (cfg_on && (!std::isfinite(o.guidance) || (s->g.Nt > 0 && !o.txt_null)))
+    return Status::arg("guidance needs a finite scale and txt_null");
+  if (buf->ws_bytes < workspace_layout(s->g, cfg_on ? 2 * B : B).total)
     return Status::make(DC_ERR_WORKSPACE, "workspace smaller than dc_workspace_bytes()");
   if (!w->blocks) return Status::arg("weights->blocks is NULL");
   s->cfg = *cfg;
   s->blocks.assign(w->blocks, w->blocks + s->g.L);
   s->w = *w;
   s->w.blocks = s->blocks.data();
+  s->cfg_on = cfg_on;
+  s->guidance = o.guidance;
+  s->txt_null = o.txt_null;
+  if (o.w_low) {
+    if (!o.w_low->blocks || !o.mod_low) return Status::arg("w_low->blocks and mod_low must be set");
+    if (o.k_switch < 2 || o.k_switch > problems[0].K) return Status::arg("k_switch must be in 2..K");
+    s->two = true;
+    s->k_switch = o.k_switch;
+    s->mod_low = o.mod_low;
+    s->blocks_low.assign(o.w_low->blocks, o.w_low->blocks + s->g.L);
+    s->w_low = *o.w_low;
+    s->w_low.blocks = s->blocks_low.data();
+  }
   s->B = B;
   s->K = problems[0].K;
   s->buf = *buf;
@@ -122,6 +149,8 @@ Status create(const dc_model_cfg* cfg, const dc_model_weights* w, int32_t B,
     if (p.start_step != 1 || p.spent_q != 0 || p.spent_n != 0)
       return Status::arg("initial problems must start at step 1 with nothing spent");
     DC_TRY(validate_problem(p));
+    if (s->two && (!p.segment || p.segment[s->k_switch - 1] == p.segment[s->k_switch - 2]))
+      return Status::arg("with two experts every scene's segment must change at k_switch");
     Scene& sc = s->scenes[size_t(b)];
     sc.prob.assign(p);
     DC_TRY(scene_tables(sc.prob.p, sc.tables));
@@ -131,6 +160,9 @@ Status create(const dc_model_cfg* cfg, const dc_model_weights* w, int32_t B,
   }
   DC_HIP(hipHostMalloc(reinterpret_cast<void**>(&s->host_sums), sizeof(double) * 4 * B));
   DC_TRY(time_modulation(s->g, &s->w, s->sigmas.data(), s->K, buf->mod, buf->ws, buf->ws_bytes, stream));
+  if (s->two)
+    DC_TRY(time_modulation(s->g, &s->w_low, s->sigmas.data(), s->K, s->mod_low, buf->ws,
+                           buf->ws_bytes, stream));
   *out = s.release();
   return Status::ok();
 }
@@ -144,13 +176,28 @@ Status step(dc_sampler* s, int k, hipStream_t st, uint8_t* realized, double* dri
   const dc_buffers& bf = s->buf;
   const int B = s->B;
   const size_t mstride = size_t(g.L + 1) * 6 * g.d;
-  const float* mod_k = bf.mod + size_t(k - 1) * mstride;
+  // the expert of this step
+  const bool low = s->two && k >= s->k_switch;
+  const dc_model_weights* W = low ? &s->w_low : &s->w;
+  const std::vector<dc_block_weights>& blocks = low ? s->blocks_low : s->blocks;
+  const float* mod_k = (low ? s->mod_low : bf.mod) + size_t(k - 1) * mstride;
+  const size_t row_stride = size_t(g.N) * g.d;            // one entry of h_in / h
+  // with guidance, scene b's unconditional branch is entry B + b of h_in, h, resid
+  auto with_branches = [&](const std::vector<int32_t>& v) {
+    std::vector<int32_t> r(v);
+    if (s->cfg_on)
+      for (int32_t b : v) r.push_back(B + b);
+    return r;
+  };
 
   IdxList all;
   std::vector<int32_t> ids(static_cast<size_t>(B));
   for (int b = 0; b < B; ++b) ids[size_t(b)] = b;
   DC_TRY(make_idx(ids.data(), B, all));
-  DC_TRY(patch_embed(g, &s->w, bf.x, bf.txt, bf.h_in, all, bf.ws, bf.ws_bytes, st));
+  DC_TRY(patch_embed(g, W, bf.x, bf.txt, bf.h_in, all, bf.ws, bf.ws_bytes, st));
+  if (s->cfg_on)
+    DC_TRY(patch_embed(g, W, bf.x, s->txt_null, bf.h_in + size_t(B) * row_stride, all, bf.ws,
+                       bf.ws_bytes, st));
 
   // planned reuses: observe the drift before any backbone call
   std::vector<int32_t> planned, refresh, reuse, vetoed;
@@ -182,29 +229,37 @@ Status step(dc_sampler* s, int k, hipStream_t st, uint8_t* realized, double* dri
   for (int b = 0; b < B; ++b) (accept[size_t(b)] ? reuse : refresh).push_back(b);
 
   if (!refresh.empty()) {
-    IdxList il;
+    IdxList il, ilb;
     DC_TRY(make_idx(refresh.data(), int(refresh.size()), il));
+    const std::vector<int32_t> rb = with_branches(refresh);
+    DC_TRY(make_idx(rb.data(), int(rb.size()), ilb));
     DC_TRY(drift_call(g, bf.h_in, mod_k, bf.u_ref, 1, nullptr, il, bf.ws, bf.ws_bytes, st));
-    for (int b : refresh)
-      DC_TRY(copy_rows(bf.h_in + size_t(b) * g.N * g.d, bf.h + size_t(b) * g.N * g.d,
-                       size_t(g.N) * g.d, st));
+    for (int b : rb)
+      DC_TRY(copy_rows(bf.h_in + size_t(b) * row_stride, bf.h + size_t(b) * row_stride, row_stride, st));
     for (int l = 0; l < g.L; ++l)
-      DC_TRY(block_forward(g, &s->blocks[size_t(l)], mod_k + size_t(l) * 6 * g.d, bf.h, il, bf.ws,
+      DC_TRY(block_forward(g, &blocks[size_t(l)], mod_k + size_t(l) * 6 * g.d, bf.h, ilb, bf.ws,
                            bf.ws_bytes, st));
     {
       ProfScope ps(KClass::kCacheStore, st);
-      DC_TRY(cache_store(bf.h, bf.h_in, bf.resid, il, g, st));
+      DC_TRY(cache_store(bf.h, bf.h_in, bf.resid, ilb, g, st));
     }
   }
   if (!reuse.empty()) {
     IdxList il;
-    DC_TRY(make_idx(reuse.data(), int(reuse.size()), il));
+    const std::vector<int32_t> rb = with_branches(reuse);
+    DC_TRY(make_idx(rb.data(), int(rb.size()), il));
     ProfScope ps(KClass::kCacheApply, st);
     DC_TRY(cache_apply(bf.h_in, bf.resid, bf.h, il, g, st));
   }
-  const float dsig = float(s->sigmas[size_t(k)] - s->sigmas[size_t(k - 1)]);
-  DC_TRY(head_euler(g, &s->w, mod_k + size_t(g.L) * 6 * g.d, bf.h, bf.x, dsig, all, bf.ws,
-                    bf.ws_bytes, st));
+  // x += dsig v, with guidance v = v_u + w (v_c - v_u) = w v_c + (1 - w) v_u: the update is
+  // linear in v, so each branch's head adds its share
+  const double dsig = s->sigmas[size_t(k)] - s->sigmas[size_t(k - 1)];
+  const float* head_mod = mod_k + size_t(g.L) * 6 * g.d;
+  DC_TRY(head_euler(g, W, head_mod, bf.h, bf.x, float(s->cfg_on ? dsig * s->guidance : dsig), all,
+                    bf.ws, bf.ws_bytes, st));
+  if (s->cfg_on)
+    DC_TRY(head_euler(g, W, head_mod, bf.h + size_t(B) * row_stride, bf.x,
+                      float(dsig * (1.0 - double(s->guidance))), all, bf.ws, bf.ws_bytes, st));
 
   // controller state
   for (int b = 0; b < B; ++b) {
@@ -251,7 +306,23 @@ dc_status dc_sampler_create(const dc_model_cfg* cfg, const dc_model_weights* w, 
                             const dc_buffers* buf, int32_t drift_metric, hipStream_t stream,
                             dc_sampler** out) {
   try {
-    Status st = create(cfg, w, B, problems, sigmas, buf, drift_metric, stream, out);
+    dc_sampler_opts o{};
+    o.drift_metric = drift_metric;
+    Status st = create(cfg, w, B, problems, sigmas, buf, o, stream, out);
+    return st ? DC_OK : fail(st);
+  } catch (const std::exception& e) {
+    return fail(Status::arg(std::string("exception: ") + e.what()));
+  }
+}
+
+dc_status dc_sampler_create_ex(const dc_model_cfg* cfg, const dc_model_weights* w, int32_t B,
+                               const dc_sched_problem* problems, const double* sigmas,
+                               const dc_buffers* buf, const dc_sampler_opts* opts,
+                               hipStream_t stream, dc_sampler** out) {
+  try {
+    dc_sampler_opts o{};
+    if (opts) o = *opts;
+    Status st = create(cfg, w, B, problems, sigmas, buf, o, stream, out);
     return st ? DC_OK : fail(st);
   } catch (const std::exception& e) {
     return fail(Status::arg(std::string("exception: ") + e.what()));

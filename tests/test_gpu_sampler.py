@@ -88,6 +88,68 @@ def test_tiny_batch_masked_dispatch_matches_oracle_per_scene(api, tiny_model):
     assert rs[:, 3].sum() == 0                    # outside the support: full inference
 
 
+def _run_variant(api, dm, w, probs, x1, txt, **kw):
+    import torch
+    smp = api.Sampler(dm, probs, I.sigmas(w.K), torch.from_numpy(x1), torch.from_numpy(txt), **kw)
+    rs, ds = smp.run()
+    torch.cuda.synchronize()
+    x = smp.x.cpu().numpy()
+    plans = [smp.plan(b) for b in range(len(probs))]
+    smp.close()
+    return x, rs, ds, plans
+
+
+@pytest.mark.parametrize("thr", [I.NO_VETO, 0.045])
+def test_tiny_guidance_branches_match_oracle(api, tiny_model, thr):
+    """Guidance branches with separate caches (Sec. 3.2, last paragraph), two scenes:
+    entries B + b of h_in, h and the cache are the unconditional branches."""
+    import torch
+    W, dm = tiny_model
+    w = TINY
+    motions = [w.motions[0], I.Motion(2.0, 0.1)]
+    probs = [I.scene_problem(w, m, thr=thr) for m in motions]
+    x1 = np.stack([I.latent(w.model, 1, s) for s in range(2)])
+    txt = np.stack([I.text(w.model, 1, s) for s in range(2)])
+    txt_null = np.stack([I.text(w.model, 1, 10 + s) for s in range(2)])
+    wg = 3.0
+    say("tiny guidance thr", thr)
+    x, rs, ds, plans = _run_variant(api, dm, w, probs, x1, txt, guidance=(wg, torch.from_numpy(txt_null)))
+    for s in range(2):
+        ref = runtime.sample(W, x1[s], txt[s], I.sigmas(w.K), probs[s], guidance=wg, txt_null=txt_null[s])
+        assert rs[:, s].tolist() == ref.realized
+        assert plans[s][0].tolist() == ref.plan
+        err = rel_l2(x[s], ref.x)
+        say("guidance scene", s, "rel-L2", err, "mask", rs[:, s].tolist())
+        assert err <= 1e-4
+    assert rs.sum() > 0
+
+
+def test_tiny_two_experts_match_oracle(api, tiny_model, dev):
+    """A high-noise and a low-noise expert split at step 6 (segment change there): no
+    cached entry crosses the switch, and each step runs its own expert's network."""
+    W, dm = tiny_model
+    w = TINY
+    ks = 6
+    W_low = I.Weights(w.model, w.cfg_id + 50)
+    dm_low = api.DeviceModel(W_low, dev)
+    seg = np.array([0] * (ks - 1) + [1] * (w.K - ks + 1), np.int32)
+    p = I.scene_problem(w, w.motions[0]).replace(segment=seg)
+    x1, txt = I.latent(w.model, 1, 0), I.text(w.model, 1, 0)
+    say("tiny two experts")
+    x, rs, ds, plans = _run_variant(api, dm, w, [p], x1[None], txt[None], low_expert=(dm_low, ks))
+    ref = runtime.sample(W, x1, txt, I.sigmas(w.K), p, W_low=W_low, k_switch=ks)
+    assert rs[:, 0].tolist() == ref.realized
+    assert rs[ks - 1, 0] == 0 and sum(ref.realized) > 0
+    err = rel_l2(x[0], ref.x)
+    say("two experts rel-L2", err, "mask", rs[:, 0].tolist())
+    assert err <= 1e-4
+    # a problem without the segment change is refused
+    import torch
+    with pytest.raises(api.L.DriveCacheError):
+        api.Sampler(dm, [I.scene_problem(w, w.motions[0])], I.sigmas(w.K), torch.from_numpy(x1[None]),
+                    torch.from_numpy(txt[None]), low_expert=(dm_low, ks))
+
+
 def test_tiny_veto_everything_equals_all_refresh(api, tiny_model):
     w = TINY
     _, dm = tiny_model
