@@ -7,6 +7,8 @@ tiles and query blocks with a ragged last one (328), the fp32 path at a
 ragged count (95), and 3,597 tokens x 30 heads, where the attention's query
 blocks outnumber the resident workgroups by just over three rounds on MI355X, so
 the last partial round runs as split key halves merged by the combine kernel.
+The fused head's extremes: one video token (one partial token tile) at d = 256
+(one 32-wide chunk per wave) and d = 2048 (eight chunks per wave).
 Also: empty index lists leave every buffer untouched."""
 import numpy as np
 import pytest
@@ -31,6 +33,8 @@ EDGE = {
     "bf16-N328": (_shape(384, 6, 64, 1536, (5, 14, 18), 13, "bf16"), 94),
     "f32-N95": (_shape(256, 4, 64, 1024, (3, 10, 12), 5, "f32"), 95),
     "bf16-N3597-h30-split": (_shape(1920, 30, 64, 7680, (10, 32, 44), 77, "bf16"), 96),
+    "bf16-N1-d256": (_shape(256, 4, 64, 1024, (1, 2, 2), 3, "bf16"), 97),
+    "bf16-N40-d2048": (_shape(2048, 32, 64, 8192, (2, 8, 10), 5, "bf16"), 98),
 }
 
 
