@@ -200,6 +200,40 @@ def test_mid_bf16_sample_matches_stored_oracle(api, dev):
     assert err <= 2e-2
 
 
+def test_mid_bf16_legality_variants_reduce_to_the_plain_sampler(api, dev):
+    """The bf16 kernels through the variant paths at the 12-block shape: guidance with
+    identical branches follows the plain sample (same decisions; two head updates in
+    place of one change only the rounding of x), and the same weights uploaded twice as
+    both experts equal the plain sample on the segmented problem bit for bit."""
+    import torch
+    name = "dit-12x1152-bf16"
+    w = I.WORKLOADS[name]
+    cal = [I.scene_problem(w, m) for m in I.calibration_motions(32)]
+    tau = api.dc_select_tau(cal, w.rho)
+    W = I.Weights(w.model, w.cfg_id)
+    say("upload", name, "twice")
+    dm, dm2 = api.DeviceModel(W, dev), api.DeviceModel(W, dev)
+    x1, txt = I.latent(w.model, w.cfg_id, 0)[None], I.text(w.model, w.cfg_id, 0)[None]
+    p = I.scene_problem(w, w.motions[0], tau_q=tau)
+    say("plain", name)
+    x0, r0, _, _ = run_gpu(api, dm, w, [p], x1, txt)
+    say("guidance with identical branches", name)
+    xg, rg, _, _ = _run_variant(api, dm, w, [p], x1, txt, guidance=(3.0, torch.from_numpy(txt)))
+    assert rg[:, 0].tolist() == r0[:, 0].tolist() and r0.sum() > 0
+    # x + 3 dsig v - 2 dsig v against x + dsig v: fp32 rounding of x at every step, carried
+    # through 30 steps of the network (the bf16 sample itself sits 2.3e-4 from the fp64 oracle)
+    assert rel_l2(xg[0], x0[0]) < 2e-3
+    ks = w.K // 2
+    seg = np.array([0] * (ks - 1) + [1] * (w.K - ks + 1), np.int32)
+    ps = p.replace(segment=seg)
+    say("segmented plain", name)
+    xs, rs_, _, _ = run_gpu(api, dm, w, [ps], x1, txt)
+    say("two experts, same weights", name)
+    xe, re_, _, _ = _run_variant(api, dm, w, [ps], x1, txt, low_expert=(dm2, ks))
+    assert re_[:, 0].tolist() == rs_[:, 0].tolist() and re_[ks - 1, 0] == 0
+    assert np.array_equal(xe, xs)
+
+
 @pytest.mark.parametrize("name", ["dit-30x1920-bf16"])
 def test_full_size_schedule_and_batch_dispatch(api, dev, name):
     """Full 17,776-token shape, first 6 steps: the sampler's plan is the oracle's
