@@ -159,7 +159,10 @@ dc_status dc_drift_l1(const dc_model_cfg* cfg, const float* h_in, const float* m
 
 /* Output interface H_k and the sampler update (Eq. 1): y = LN(g)(1+scale_f)+shift_f
  * on the video rows of g (f32 [B, N, d]), v = unpatchify(y w_head^T + b_head),
- * x[b] += dsigma * v.  head_mod: f32 [2, d] (shift_f, scale_f); x: f32 [B, C, T, H, W]. */
+ * x[b] += dsigma * v.  head_mod: f32 [2, d] (shift_f, scale_f); x: f32 [B, C, T, H, W].
+ * bf16 models with hidden <= 2048 run one pass over g with the projection operand
+ * split into two bf16 halves (about fp32 accuracy); wider bf16 models round y to
+ * bf16 before the projection. */
 dc_status dc_head_euler(const dc_model_cfg* cfg, const dc_model_weights* w,
                         const float* head_mod, const float* g, float* x, float dsigma,
                         const int32_t* idx, int32_t n, void* ws, size_t ws_bytes,
