@@ -43,3 +43,56 @@ def test_errors_are_reported_not_raised():
     # a shape check fails before anything touches a device
     rc = lib.dc_block_forward(C.byref(bad), None, None, None, None, 0, None, 0, None)
     assert rc == _lib.DC_ERR_SHAPE
+
+
+def test_sampler_options_are_validated_before_any_device_work():
+    """dc_sampler_create_ex refuses bad legality options on the host (the pointers below
+    are never dereferenced on the device: every case fails before the first device call)."""
+    import ctypes as C
+    import numpy as np
+    from paper_2608_16354_amd import api
+    from paper_2608_16354_amd import inputs as I
+    lib = _lib.load()
+    w = I.WORKLOADS["dit-tiny-f32"]
+    m = w.model
+    cfg = _lib.ModelCfg(m.n_blocks, m.hidden, m.heads, m.head_dim, m.mlp_hidden, m.lat_c, m.lat_t,
+                        m.lat_h, m.lat_w, m.patch, m.n_txt, 0, m.ln_eps)
+    fake = C.c_void_p(0x1000)
+    blocks = (_lib.BlockWeights * m.n_blocks)()
+    weights = _lib.ModelWeights()
+    weights.blocks = C.cast(blocks, C.POINTER(_lib.BlockWeights))
+    ws = lib.dc_workspace_bytes(C.byref(cfg), 2)
+    bufs = _lib.Buffers(fake, fake, fake, fake, fake, fake, fake, fake, fake, ws)
+    sig = np.ascontiguousarray(I.sigmas(w.K))
+    sigp = sig.ctypes.data_as(C.POINTER(C.c_double))
+
+    def create(problems, opts, B=1):
+        cps = [api._CProblem(p) for p in problems]
+        arr = (_lib.SchedProblem * len(cps))(*[c.c for c in cps])
+        h = C.c_void_p()
+        rc = lib.dc_sampler_create_ex(C.byref(cfg), C.byref(weights), B, arr, sigp, C.byref(bufs),
+                                      C.byref(opts), None, C.byref(h))
+        assert not h.value
+        return rc, lib.dc_last_error()
+
+    p = I.scene_problem(w, w.motions[0])
+    # guidance: a non-finite scale, and more than half the batch limit
+    o = _lib.SamplerOpts(); o.cfg = 1; o.guidance = float("nan"); o.txt_null = 0x1000
+    assert create([p], o)[0] == _lib.DC_ERR_ARG
+    o = _lib.SamplerOpts(); o.cfg = 1; o.guidance = 2.0; o.txt_null = 0x1000
+    assert create([p] * 33, o, B=33)[0] == _lib.DC_ERR_ARG
+    # two experts: k_switch out of range, no modulation table, no segment change
+    low = _lib.ModelWeights()
+    low.blocks = C.cast(blocks, C.POINTER(_lib.BlockWeights))
+    o = _lib.SamplerOpts(); o.w_low = C.pointer(low); o.mod_low = 0x1000; o.k_switch = 1
+    assert create([p], o)[0] == _lib.DC_ERR_ARG
+    o.k_switch = w.K + 1
+    assert create([p], o)[0] == _lib.DC_ERR_ARG
+    o.k_switch = 5; o.mod_low = None
+    assert create([p], o)[0] == _lib.DC_ERR_ARG
+    o.mod_low = 0x1000
+    rc, msg = create([p], o)
+    assert rc == _lib.DC_ERR_ARG and b"segment" in msg
+    # an unknown option value
+    o = _lib.SamplerOpts(); o.cfg = 2
+    assert create([p], o)[0] == _lib.DC_ERR_ARG
