@@ -2,8 +2,9 @@
 //
 // bf16 block GEMMs (QKV, out-projection, MLP up / down): v_mfma_f32_32x32x16_bf16,
 // 8 waves, block tile 384 x 192 x 64 (QKV, out-projection, MLP down: fewer operand
-// lines per FLOP, the L1 miss queue being the limit) or 256 x 192 x 64 (MLP up, whose
-// 40 column tiles quantise better), tiles fed global -> LDS by LDS-DMA into two
+// lines per FLOP, the L1 miss queue being the limit) or 320 x 256 x 64 (MLP up: still
+// fewer lines per FLOP, and its 30 column tiles quantise well over the rounds), tiles
+// fed global -> LDS by LDS-DMA into two
 // stages (the refill of the next k-step interleaved with this k-step's MFMAs),
 // XOR-swizzled 128-byte rows, one barrier per k-step, XCD-aware tile order;
 // epilogues take one accumulator column at a time.
@@ -515,8 +516,9 @@ Status launch_dma(const uint16_t* A, int lda, const uint16_t* W, int ldw, int M,
 // (token block, column chunk) are dealt so that an XCD runs every column chunk of
 // a contiguous range of token blocks, so each XCD's L2 fetches only its own part
 // of the latent.  Each wave's 32 x 32 result tiles go through LDS, so the output
-// rows leave as 16-byte stores (8 rows x 128 bytes per instruction) and the
-// positional rows arrive as 8-byte loads.
+// rows leave as 16-byte stores (8 rows x 128 bytes per instruction; ordinary stores:
+// the drift check and the first block read h_in right after, partly from the caches)
+// and the positional rows arrive as 8-byte loads.
 // ---------------------------------------------------------------------------
 struct PatchGeo { int T, Hl, Wl, p, lp, Hp, Wp; };   // lp = log2(p)
 
@@ -624,7 +626,7 @@ __global__ void __launch_bounds__(512) k_patch_embed_bf16(const float* __restric
       o.y = (a.y + b4.y) + __uint_as_float(pv[q].x & 0xFFFF0000u);
       o.z = (a.z + b4.z) + __uint_as_float(pv[q].y << 16);
       o.w = (a.w + b4.w) + __uint_as_float(pv[q].y & 0xFFFF0000u);
-      if (mm < Nv) store_nt(out + size_t(mm) * d + nc, o);
+      if (mm < Nv) *reinterpret_cast<float4*>(out + size_t(mm) * d + nc) = o;
     }
     if (tile < 3) {
 #pragma unroll
@@ -745,7 +747,7 @@ Status gemm_bf16_gate_residual(const uint16_t* A, int lda, const uint16_t* W, co
 
 Status gemm_bf16_gelu(const uint16_t* A, int lda, const uint16_t* W, const float* bias,
                       uint16_t* out, int ldo, int M, int N, int K, hipStream_t s) {
-  return launch_dma<256, 192, 4, 2, 2>(A, lda, W, K, M, N, K, EpiGeluBf16{bias, out, ldo}, s);
+  return launch_dma<320, 256, 2, 4, 2>(A, lda, W, K, M, N, K, EpiGeluBf16{bias, out, ldo}, s);
 }
 
 Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float* bias, float* x,
