@@ -15,7 +15,7 @@
 // tokens, 16 at a time.  Its 8 waves split d into 32-wide chunks (at d = 1920 seven
 // or eight each) and keep their chunks of W_head in registers for the whole kernel;
 // a wave streams its part of the 16 token rows (64 contiguous bytes per row and
-// instruction) four chunks ahead through a register ring, so about 128 KB per
+// instruction) four chunks ahead through a register ring, so about 64 KB per
 // compute unit is in flight.  The shift K is the row's first value (a sample of the
 // row, so y stays small next to g when the row mean is large); cs and shw are computed
 // once per workgroup on the matrix cores.  Per token tile the waves leave their
