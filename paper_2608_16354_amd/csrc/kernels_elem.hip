@@ -81,26 +81,32 @@ __device__ inline float4 load4(const void* in, size_t e, bool bf) {
   return *reinterpret_cast<const float4*>(static_cast<const float*>(in) + e);
 }
 
-// a = LN(x)(1 + scale) + shift, one wavefront per row (NV float4 per lane).
+// a = LN(x)(1 + scale) + shift, one wavefront per row (NV float4 per lane).  shift and
+// scale go through LDS once per block of four rows, so the L1 and L2 see each row's data
+// and not four more copies of the modulation vectors (-8 % at 17,776 x 1920).
 template <int NV>
 __global__ void __launch_bounds__(256) k_ln_modulate(const float* __restrict__ x, int rows, int ldx,
                                                      const float* __restrict__ shift,
                                                      const float* __restrict__ scale, void* out,
                                                      int ldo, int d, float eps, bool bf) {
+  __shared__ float4 s_sh[NV * kWave], s_sc[NV * kWave];
+  const int n4 = d >> 2;
+  for (int i = threadIdx.x; i < n4; i += 256) {
+    s_sh[i] = reinterpret_cast<const float4*>(shift)[i];
+    s_sc[i] = reinterpret_cast<const float4*>(scale)[i];
+  }
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const int n4 = d >> 2;
   float4 v[NV];
-  load_row_nv<NV>(x + size_t(row) * ldx, n4, lane, v);
+  load_row_nv<NV>(x + size_t(min(row, rows - 1)) * ldx, n4, lane, v);
+  __syncthreads();
+  if (row >= rows) return;
   float mean, rstd;
   row_stats_nv<NV>(v, n4, lane, eps, mean, rstd);
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = min(lane + i * kWave, n4 - 1);
-    const float4 sh = reinterpret_cast<const float4*>(shift)[c];
-    const float4 sc = reinterpret_cast<const float4*>(scale)[c];
-    const float4 u = modulate4(v[i], mean, rstd, sh, sc);
+    const float4 u = modulate4(v[i], mean, rstd, s_sh[c], s_sc[c]);
     if (lane + i * kWave < n4) store4(out, size_t(row) * ldo + 4 * c, u, bf);
   }
 }
