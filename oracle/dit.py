@@ -29,10 +29,39 @@ architectural detail is a reading, listed here:
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
+from threadpoolctl import threadpool_limits
 
 F = np.float64
+
+
+def _workers():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _by_rows(fn, x, *args, min_rows=4096):
+    """fn(x, *args) for a row-wise fn (each output row depends on its input row only),
+    evaluated on row ranges in worker threads; the values are those of one call."""
+    n = x.shape[0]
+    nw = _workers()
+    if n < min_rows or nw == 1:
+        return fn(x, *args)
+    bounds = np.linspace(0, n, nw + 1).astype(int)
+    out = np.empty(x.shape, F)
+
+    def run(i):
+        out[bounds[i]: bounds[i + 1]] = fn(x[bounds[i]: bounds[i + 1]], *args)
+
+    with ThreadPoolExecutor(nw) as ex:
+        list(ex.map(run, range(nw)))
+    return out
 
 
 def silu(x):
@@ -166,26 +195,47 @@ def attention(q, k, v, heads, chunk=2048):
     return out
 
 
-def block(P: Params, l, mod6, h, rows=None):
-    """One transformer block on h [N, d]; returns the updated rows (all rows, or
-    only `rows` -- every row's keys and values are still used)."""
-    m = P.m
-    d = m.hidden
-    eps = m.ln_eps
-    shift1, scale1, gate1, shift2, scale2, gate2 = mod6
-    a = modulate(h, shift1, scale1, eps)
+def _block_rows(P: Params, l, mod6, h, a, k, v):
+    """The part of block l after the keys and values: rows h, with modulated input a,
+    attend to every row's k, v; each output row depends on its own row only."""
+    d = P.m.hidden
+    eps = P.m.ln_eps
+    _, _, gate1, shift2, scale2, gate2 = mod6
     wq, bq = P.b(l, "w_qkv"), P.b(l, "b_qkv")
-    kv = a @ wq[d:].T + bq[d:]                 # keys and values of every row
-    k, v = kv[:, :d], kv[:, d:]
-    sel = slice(None) if rows is None else rows
-    q = a[sel] @ wq[:d].T + bq[:d]
-    hr = h[sel].copy()
-    o = attention(q, k, v, m.heads)
-    hr = hr + gate1 * (o @ P.b(l, "w_o").T + P.b(l, "b_o"))
+    q = a @ wq[:d].T + bq[:d]
+    o = attention(q, k, v, P.m.heads)
+    hr = h + gate1 * (o @ P.b(l, "w_o").T + P.b(l, "b_o"))
     a2 = modulate(hr, shift2, scale2, eps)
     z = gelu_tanh(a2 @ P.b(l, "w_1").T + P.b(l, "b_1"))
-    hr = hr + gate2 * (z @ P.b(l, "w_2").T + P.b(l, "b_2"))
-    return hr
+    return hr + gate2 * (z @ P.b(l, "w_2").T + P.b(l, "b_2"))
+
+
+def block(P: Params, l, mod6, h, rows=None, chunk=256):
+    """One transformer block on h [N, d]; returns the updated rows (all rows, or
+    only `rows` -- every row's keys and values are still used).
+    Given the keys and values, rows are independent: they are evaluated in chunks
+    of `chunk` rows in worker threads (one BLAS thread each), only to use the
+    host's cores with cache-sized temporaries."""
+    d = P.m.hidden
+    shift1, scale1 = mod6[0], mod6[1]
+    a = _by_rows(modulate, h, shift1, scale1, P.m.ln_eps)
+    wq, bq = P.b(l, "w_qkv"), P.b(l, "b_qkv")
+    kv = a @ wq[d:].T + bq[d:]                 # keys and values of every row
+    k = np.ascontiguousarray(kv[:, :d])
+    v = np.ascontiguousarray(kv[:, d:])
+    sel = np.arange(h.shape[0]) if rows is None else np.arange(h.shape[0])[rows]
+    out = np.empty((len(sel), d), F)
+    starts = range(0, len(sel), chunk)
+
+    def run(s):
+        rr = sel[s: s + chunk]
+        out[s: s + chunk] = _block_rows(P, l, mod6, h[rr], a[rr], k, v)
+
+    for name in ("w_o", "b_o", "w_1", "b_1", "w_2", "b_2"):
+        P.b(l, name)                           # load once, before the threads share P
+    with threadpool_limits(1), ThreadPoolExecutor(_workers()) as ex:
+        list(ex.map(run, starts))
+    return out
 
 
 def backbone(P: Params, mods, h_in):

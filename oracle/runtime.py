@@ -79,7 +79,7 @@ def drift_value(sums, eps, metric="l1"):
 
 
 def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
-           W_low=None, k_switch=None, guidance=None, txt_null=None):
+           W_low=None, k_switch=None, guidance=None, txt_null=None, steps=None, on_step=None):
     """One cached K-step sample of one scene.
 
     W: `Weights`; x1 [C,T,H,W]; txt [n_txt, d]; sigmas [K+1]; prob: `SchedProblem`.
@@ -88,7 +88,10 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
     (exercises the veto path).
     W_low, k_switch: the low-noise expert and the first step it runs (prob.segment
     must change at k_switch).  guidance, txt_null: the guidance scale w and the
-    unconditional text; the branches keep separate caches."""
+    unconditional text; the branches keep separate caches.
+    steps: stop after this many steps (default K); the result then holds x_{steps+1}.
+    on_step(k, x, records, plan): called after each step with the latent x_{k+1}, the
+    records so far and the current plan (for writing intermediate results)."""
     experts = [dit.Params(W)]
     if W_low is not None:
         if prob.segment is None or prob.segment[k_switch - 1] == prob.segment[k_switch - 2]:
@@ -110,7 +113,7 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
     r_u = None
     u_ref = None
     records = []
-    for k in range(1, K + 1):
+    for k in range(1, (K if steps is None else min(steps, K)) + 1):
         P = experts[1] if (W_low is not None and k >= k_switch) else experts[0]
         mods, head_mod = dit.step_modulation(P, sigmas[k - 1])
         h_in = dit.embed(P, x, txt)
@@ -158,4 +161,6 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
             v_u = dit.head(P, head_mod, g_u)
             v = v_u + guidance * (v - v_u)
         x = dit.euler(x, v, sigmas[k - 1], sigmas[k])
+        if on_step is not None:
+            on_step(k, x, records, mask)
     return SampleResult(x, records, plans, C, mask)

@@ -1,9 +1,19 @@
-"""Write the oracle's full cached sample of the 12-block bf16 workload
-(dit-12x1152-bf16: 3,584 + 120 tokens, 30 steps, stationary plan) for the GPU
-parity test.  Calls only the oracle and the seeded input generator.
+"""Write the oracle's cached sample of a workload for the GPU parity tests.
+Calls only the oracle and the seeded input generator.
 
-    python tests/golden/make_oracle_artifacts.py
+    python tests/golden/make_oracle_artifacts.py dit-12x1152-bf16
+    python tests/golden/make_oracle_artifacts.py dit-12x1152-bf16 --thr 0.05 --tag veto
+    python tests/golden/make_oracle_artifacts.py dit-30x1920-bf16 --every-step
+
+The file `oracle_<workload>[-<tag>].npz` holds the latent after `steps` steps
+(float32), the realized, planned and vetoed flags of every step, every observed
+drift (rel-L1 and rel-L2; NaN where no check ran) with the threshold it was
+compared with, the plan as it stood after the last step, the veto count, the
+charge, the budget tau and a fingerprint of the generated inputs.  With
+--every-step the file is rewritten after each step (a long run leaves a valid
+truncated artefact at every point).
 """
+import argparse
 import hashlib
 import os
 import sys
@@ -30,21 +40,68 @@ def fingerprint(w):
     return h.hexdigest()
 
 
-def main(name="dit-12x1152-bf16"):
-    w = I.WORKLOADS[name]
+def artefact_path(name, tag=None):
+    return os.path.join(HERE, f"oracle_{name}{'' if not tag else '-' + tag}.npz")
+
+
+def _write(path, name, thr, tau, fp, k, x, records, plan, seconds):
+    nan = np.nan
+    rec = {
+        "x": x.astype(np.float32),
+        "steps": np.int32(k),
+        "realized": np.array([r.realized for r in records], np.uint8),
+        "planned": np.array([r.planned for r in records], np.uint8),
+        "vetoed": np.array([bool(r.vetoed) for r in records], np.uint8),
+        "drift": np.array([nan if r.drift is None else r.drift for r in records]),
+        "drift_l2": np.array([nan if r.drift_l2 is None else r.drift_l2 for r in records]),
+        "threshold": np.array([nan if r.threshold is None else r.threshold for r in records]),
+        "plan": np.array(plan, np.uint8),
+        "n_veto": np.int32(sum(bool(r.vetoed) for r in records)),
+        "tau_q": np.int64(tau),
+        "thr": np.float64(thr),
+        "fingerprint": np.array(fp),
+        "workload": np.array(name),
+        "oracle_seconds": np.float64(seconds),
+    }
+    tmp = path + ".tmp.npz"
+    np.savez(tmp, **rec)
+    os.replace(tmp, path)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("name", nargs="?", default="dit-12x1152-bf16")
+    ap.add_argument("--thr", type=float, default=None, help="drift threshold (default: the workload's)")
+    ap.add_argument("--tag", default=None, help="suffix of the file name")
+    ap.add_argument("--steps", type=int, default=None, help="stop after this many steps")
+    ap.add_argument("--every-step", action="store_true", help="rewrite the file after every step")
+    a = ap.parse_args(argv)
+    w = I.WORKLOADS[a.name]
+    thr = w.thr if a.thr is None else a.thr
     cal = [I.scene_problem(w, m) for m in I.calibration_motions(32)]
     tau = budget.select_tau(cal, w.rho)
-    p = I.scene_problem(w, w.motions[0], tau_q=tau)
+    p = I.scene_problem(w, w.motions[0], tau_q=tau, thr=thr)
     W = I.Weights(w.model, w.cfg_id)
+    fp = fingerprint(w)
+    path = artefact_path(a.name, a.tag)
     t0 = time.time()
+
+    def on_step(k, x, records, plan):
+        W.drop()          # the oracle keeps its own float64 copies of every tensor it used
+        r = records[-1]
+        d = "" if r.drift is None else f" drift {r.drift:.6f} thr {r.threshold:.4f}"
+        print(f"{a.name} step {k}: {'reuse' if r.realized else 'full'}{' (vetoed)' if r.vetoed else ''}"
+              f"{d}  [{time.time() - t0:.0f} s]", flush=True)
+        if a.every_step:
+            _write(path, a.name, thr, tau, fp, k, x, records, plan, time.time() - t0)
+
     res = runtime.sample(W, I.latent(w.model, w.cfg_id, 0), I.text(w.model, w.cfg_id, 0),
-                         I.sigmas(w.K), p)
-    print(f"{name}: {time.time() - t0:.1f} s, realized {''.join(map(str, res.realized))}")
-    drift = np.array([np.nan if r.drift is None else r.drift for r in res.records])
-    np.savez(os.path.join(HERE, f"oracle_{name}.npz"), x=res.x.astype(np.float32),
-             realized=np.array(res.realized, np.uint8), drift=drift, tau_q=np.int64(tau),
-             fingerprint=np.array(fingerprint(w)))
+                         I.sigmas(w.K), p, steps=a.steps, on_step=on_step)
+    k = len(res.records)
+    _write(path, a.name, thr, tau, fp, k, res.x, res.records, res.plan, time.time() - t0)
+    print(f"{a.name}: {time.time() - t0:.1f} s, {k} steps, realized "
+          f"{''.join(map(str, res.realized))}, vetoes {sum(r.vetoed for r in res.records)}")
 
 
 if __name__ == "__main__":
-    main(*sys.argv[1:])
+    main()
