@@ -228,3 +228,77 @@ def test_block_mlp_special_case_is_gated_gelu():
     got = dit.block(P, 0, mod, h) - h
     assert np.allclose(got, gate2 * z, atol=3e-3 * np.abs(gate2).max())
     assert not np.allclose(got, gate2 * a2, atol=1e-3)
+
+
+class _StubAll(_Stub):
+    def __init__(self, m, glob, blocks):
+        super().__init__(m, None)
+        self._g = glob
+        self._bl = blocks
+
+    def block(self, l, name):
+        return self._bl[l][name]
+
+    def get(self, name):
+        return self._g[name]
+
+
+def test_time_embedding_and_modulation_closed_form():
+    """Hand-built conditioning weights that reduce the timestep MLP and the shared
+    modulation projection to per-element closed forms, evaluated with scalar math:
+    W_t1 picks one sinusoid per hidden unit (a cosine for most, a scaled sine for the
+    last), W_t2 is diagonal plus one off-diagonal entry, W_m stacks +I, -3I, zero and a diagonal.  A dropped
+    SiLU, a SiLU in the wrong place, a transposed weight, a wrong [6, d] row order or
+    a missing [c; c] head offset each changes the result."""
+    m = I.ModelShape(2, 8, 2, 4, 32, 16, 1, 2, 2, 2, 0, "f32")
+    d, nf = m.hidden, m.t_freq
+    half = nf // 2
+    r = np.random.default_rng(5)
+    w_t1 = np.zeros((d, nf))
+    pick = [3 * i for i in range(d - 1)]
+    for i, f in enumerate(pick):
+        w_t1[i, f] = 1.0
+    w_t1[d - 1, half + 5] = -2.0                      # the sine of frequency 5
+    b_t1 = 0.1 * np.arange(d) - 0.3
+    diag_t2 = 0.5 * (np.arange(d) + 1)
+    b_t2 = 0.01 * np.arange(d)
+    w_m = np.zeros((6 * d, d))
+    w_m[0:d] = np.eye(d)
+    w_m[d:2 * d] = -3.0 * np.eye(d)
+    diag_m5 = r.normal(size=d)
+    w_m[5 * d:6 * d] = np.diag(diag_m5)
+    b_m = r.normal(size=6 * d)
+    head_mod = r.normal(size=(2, d))
+    offs = [r.normal(size=(6, d)) for _ in range(m.n_blocks)]
+    w_t2 = np.diag(diag_t2)
+    w_t2[0, d - 1] = 0.7                              # one off-diagonal entry: orientation matters
+    glob = {"w_t1": w_t1, "b_t1": b_t1, "w_t2": w_t2, "b_t2": b_t2,
+            "w_m": w_m, "b_m": b_m, "head_mod": head_mod}
+    P = dit.Params(_StubAll(m, glob, [{"mod_offset": o} for o in offs]))
+
+    def silu(z):
+        return z / (1.0 + math.exp(-z))
+
+    for sigma in (0.0, 0.37, 1.0):
+        t = 1000.0 * sigma
+        freq = [10000.0 ** (-i / half) for i in range(half)]
+        pre = [math.cos(t * freq[f]) + b_t1[i] for i, f in enumerate(pick)]
+        pre.append(-2.0 * math.sin(t * freq[5]) + b_t1[d - 1])
+        c = np.array([diag_t2[i] * silu(pre[i]) + b_t2[i] for i in range(d)])
+        c[0] += 0.7 * silu(pre[d - 1])
+        s = np.array([silu(ci) for ci in c])
+        mm = b_m.reshape(6, d).copy()
+        mm[0] += s
+        mm[1] += -3.0 * s
+        mm[5] += diag_m5 * s
+        assert np.allclose(dit.time_embedding(P, sigma), c, rtol=1e-13, atol=1e-14)
+        blocks, head = dit.step_modulation(P, sigma)
+        for l in range(m.n_blocks):
+            assert np.allclose(blocks[l], mm + offs[l], rtol=1e-13, atol=1e-14)
+        assert np.allclose(head, head_mod + np.stack([c, c]), rtol=1e-13, atol=1e-14)
+    # at t = 0 every cosine feature is 1 and every sine 0 (closed form of the features)
+    blocks0, _ = dit.step_modulation(P, 0.0)
+    z = 1.0 + b_t1[0]
+    zl = b_t1[d - 1]
+    c0 = diag_t2[0] * z / (1.0 + math.exp(-z)) + 0.7 * zl / (1.0 + math.exp(-zl)) + b_t2[0]
+    assert blocks0[0][0, 0] == pytest.approx(c0 / (1.0 + math.exp(-c0)) + b_m[0] + offs[0][0, 0], rel=1e-14)
