@@ -8,7 +8,10 @@ are resident in HBM before the timed region.
 
 Prints one JSON line: latent tokens x steps / s = B * N_v * K / (seconds per
 sample), the roofline of the dominant kernel (attention, timed live with
-hipEvents over the timed region) and the CPU oracle's rate on a bounded sample.
+hipEvents over the timed region), the combined GEMM + attention MFMA fraction of
+the refresh steps, the HBM rate of every reuse-path kernel, a run record (config
+hash, realized masks, vetoes, every drift with its margin to the threshold) and
+the CPU oracle's rate on a bounded sample.
 """
 import argparse
 import json
@@ -49,6 +52,28 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def gemm_flops(m):
+    """Algorithmic FLOPs of one block's four GEMMs (QKV, out-projection, MLP up and down)."""
+    N, d, F = m.n_tok, m.hidden, m.mlp_hidden
+    return 2.0 * N * d * (3 * d + d + 2 * F)
+
+
+def hbm_bytes(m):
+    """Algorithmic HBM bytes per launch (one scene) of the HBM-bound kernels: every
+    operand read once and every result written once."""
+    Nv, N, d = m.n_v, m.n_tok, m.hidden
+    e = 2 if m.dtype == "bf16" else 4
+    lat = 4 * m.lat_c * m.lat_t * m.lat_h * m.lat_w
+    return {
+        "patch_embed": Nv * d * 4 + Nv * d * e + lat,          # write h_in rows, read pos and x
+        "drift": Nv * d * (4 + e),                             # read h_in and u_ref / write u_ref
+        "cache_store": Nv * d * (4 + 4 + e),                   # read h_out, h_in; write r
+        "cache_apply": Nv * d * (4 + e + 4),                   # read h_in, r; write g
+        "head": Nv * d * 4 + 2 * lat,                          # read g; read and write x
+        "ln_modulate": N * d * (4 + e),                        # read h; write a
+    }
+
+
 def attention_flops(m):
     """Algorithmic FLOPs of one attention launch (one scene, all heads): QK^T and PV."""
     return 4.0 * m.n_tok * m.n_tok * m.hidden
@@ -59,6 +84,25 @@ def refresh_flops(m):
     N, d, F = m.n_tok, m.hidden, m.mlp_hidden
     per_block = 2.0 * N * d * (3 * d + d + 2 * F) + attention_flops(m)
     return m.n_blocks * per_block + 2.0 * 2 * m.n_v * 64 * d
+
+
+def host_info():
+    """CPU model name and NumPy's BLAS (the oracle's matrix products)."""
+    import numpy as np
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        b = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{b.get('name')} {b.get('version')}"
+    except Exception:
+        blas = "unknown"
+    return model, blas
 
 
 def cpu_baseline(w, W, schedule, budget_s=30.0):
@@ -95,13 +139,39 @@ def cpu_baseline(w, W, schedule, budget_s=30.0):
     n_ref = sum(1 for r in schedule if not r)
     n_reu = len(schedule) - n_ref
     t_sample = n_ref * (m.n_blocks * t_block + t_reuse) + n_reu * t_reuse
-    cores = len(os.sched_getaffinity(0))
+    cores = min(16, len(os.sched_getaffinity(0)))     # the oracle's worker and BLAS threads
     spent = sum(times.values()) + t_reuse
+    cpu, blas = host_info()
     return {"value": w.batch * m.n_v * w.K / (w.batch * t_sample), "unit": "latent token*steps/s",
-            "cores": cores, "kind": "oracle",
+            "cores": cores, "kind": "oracle", "dtype": "f64", "cpu_model": cpu, "blas": blas,
             "sample": (f"fp64 oracle: one block at {m.n_tok} tokens on 1024 and 4096 query rows "
                        f"({times[1024]:.1f}s, {times[4096]:.1f}s) + one full reuse step ({t_reuse:.1f}s), "
                        f"extrapolated to the {n_ref}-refresh/{n_reu}-reuse schedule; {spent:.0f}s of CPU work")}
+
+
+def run_record(api, w, probs, realized, drift, plans):
+    """Per scene: the realized mask (1 = reuse), vetoes, and every drift check with its
+    threshold dbar_{j,h} (the scene table of the run's refresh step j at age h) and its
+    margin thr - drift (negative: vetoed by the drift)."""
+    import numpy as np
+    scenes = []
+    for b, p in enumerate(probs):
+        dbar = api.dc_schedule_dp(p).dbar
+        j, age, checks = 1, 0, []
+        for k in range(1, w.K + 1):
+            d = float(drift[k - 1, b])
+            if not np.isnan(d):
+                thr = float(dbar[j - 1, age])
+                checks.append({"k": k, "drift": d, "threshold": thr, "margin": thr - d})
+            if realized[k - 1, b]:
+                age += 1
+            else:
+                j, age = k, 0
+        scenes.append({"mask": "".join(str(int(v)) for v in realized[:, b]),
+                       "n_veto": int(plans[b][1]), "charge_q": int(plans[b][2]),
+                       "min_abs_margin": min((abs(c["margin"]) for c in checks), default=None),
+                       "checks": checks})
+    return {"scenes": scenes}
 
 
 def main():
@@ -151,12 +221,17 @@ def main():
     sig = I.sigmas(w.K)
     torch.cuda.synchronize()
 
+    last = {}
+
     def one_sample():
         smp = api.Sampler(dm, probs, sig, x1, txt, bufs=bufs)
-        rs = []
+        rs, ds = [], []
         for _ in range(w.K):
-            r, _ = smp.step()
+            r, d = smp.step()
             rs.append(r)
+            ds.append(d)
+        last["plans"] = [smp.plan(b) for b in range(w.batch)]
+        last["drift"] = np.stack(ds)
         smp.close()
         return np.stack(rs)
 
@@ -164,7 +239,7 @@ def main():
         one_sample()
         torch.cuda.synchronize()
         log(f"warmup {i + 1}/{args.warmup} done")
-    prof = api.profile(["attention"]) if not args.no_profile else None
+    prof = api.profile(list(api.L.KERNEL_CLASSES)) if not args.no_profile else None
     torch.cuda.synchronize()
     if prof:
         prof.__enter__()
@@ -182,6 +257,8 @@ def main():
     value = w.batch * m.n_v * w.K / (ms_per / 1000.0)
     realized = masks[-1]
     n_refresh = int((realized == 0).sum())
+    fp = I.input_fingerprint(w)
+    record = run_record(api, w, probs, realized, last["drift"], last["plans"])
     out = {
         "metric": "latent tokens x steps / s, cached 50-step sample",
         "value": value, "unit": "latent token*steps/s", "n_gpus": 1, "steps": args.steps,
@@ -190,7 +267,9 @@ def main():
         "config": {"workload": w.name, "blocks": m.n_blocks, "hidden": m.hidden, "heads": m.heads,
                    "video_tokens": m.n_v, "text_tokens": m.n_txt, "denoise_steps": w.K,
                    "batch": w.batch, "refresh_steps": n_refresh, "reuse_steps": int(realized.sum()),
-                   "tau_q": int(tau) if tau != I.TAU_INF else None},
+                   "tau_q": int(tau) if tau != I.TAU_INF else None,
+                   "config_hash": I.config_hash(w, tau, fp)},
+        "run": record,
     }
     if prof:
         n, tot = kstats["attention"]
@@ -201,6 +280,28 @@ def main():
                            "frac": achieved / MI355X_BF16_DENSE_TFLOPS,
                            "traffic": traffic_from_profile("attention.hip"),
                            "launches": n, "avg_ms": avg_ms}
+        # refresh steps: the block GEMMs and attention together against the dense bf16 peak
+        mm = ["attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down"]
+        mm_ms = sum(kstats[c][1] for c in mm)
+        blocks_run = kstats["attention"][0]
+        if blocks_run and mm_ms > 0:
+            fl = blocks_run * (attention_flops(m) + gemm_flops(m))
+            rate = fl / (mm_ms / 1000.0) / 1e12
+            out["refresh_mfma"] = {"kernels": "block GEMMs + attention", "achieved": rate,
+                                   "peak": MI355X_BF16_DENSE_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": rate / MI355X_BF16_DENSE_TFLOPS,
+                                   "ms_per_block": mm_ms / blocks_run,
+                                   "per_kernel_avg_us": {c: 1000.0 * kstats[c][1] / max(kstats[c][0], 1)
+                                                         for c in mm}}
+        hb = hbm_bytes(m)
+        out["hbm_kernels"] = {}
+        for c, nbytes in hb.items():
+            n_c, ms_c = kstats[c]
+            if n_c:
+                gbs = nbytes / (ms_c / n_c / 1000.0) / 1e9
+                out["hbm_kernels"][c] = {"avg_us": 1000.0 * ms_c / n_c, "launches": n_c,
+                                         "algorithmic_bytes": nbytes, "GB/s": gbs,
+                                         "frac": gbs / MI355X_HBM_GBPS}
     # refresh FLOPs of the executed schedule over the whole sample time (reuse steps included)
     out["sample_tflops"] = refresh_flops(m) * n_refresh / (ms_per / 1000.0) / 1e12
     if not args.no_cpu_baseline:

@@ -221,10 +221,13 @@ Status block_forward(const Geo& g, const dc_block_weights* bw, const float* mod,
   return Status::ok();
 }
 
+// resid != NULL (bf16 models the fused head takes): the head input of sample b is
+// g = gin[b] + resid[b] on the video rows, formed inside the head kernel (reuse steps).
 Status head_euler(const Geo& g, const dc_model_weights* w, const float* head_mod, const float* gin,
                   float* x, float dsigma, const IdxList& il, void* ws, size_t ws_bytes,
-                  hipStream_t s) {
+                  hipStream_t s, const void* resid) {
   if (!w || !head_mod || !gin || !x || !w->w_head || !w->b_head) return Status::arg("NULL argument");
+  if (resid && !head_euler_fused_ok(g)) return Status::shape("head with a residual input needs the fused bf16 head");
   Workspace L;
   DC_TRY(check_ws(g, max_index(il) + 1, ws, ws_bytes, L));
   const size_t lat = size_t(g.C) * g.T * g.Hl * g.Wl;
@@ -233,7 +236,8 @@ Status head_euler(const Geo& g, const dc_model_weights* w, const float* head_mod
     const float* gb = gin + size_t(b) * g.N * g.d;
     ProfScope ps(KClass::kHead, s);
     if (head_euler_fused_ok(g)) {
-      DC_TRY(head_euler_bf16(gb, static_cast<const uint16_t*>(w->w_head), w->b_head, head_mod,
+      const uint16_t* rb = resid ? static_cast<const uint16_t*>(resid) + size_t(b) * g.Nv * g.d : nullptr;
+      DC_TRY(head_euler_bf16(gb, rb, static_cast<const uint16_t*>(w->w_head), w->b_head, head_mod,
                              head_mod + g.d, x + size_t(b) * lat, dsigma, g, s));
       continue;
     }
@@ -362,7 +366,7 @@ dc_status dc_head_euler(const dc_model_cfg* cfg, const dc_model_weights* w, cons
     IdxList il;
     DC_TRY(make_geo(cfg, g));
     DC_TRY(make_idx(idx, n, il));
-    return head_euler(g, w, head_mod, g_in, x, dsigma, il, ws, ws_bytes, stream);
+    return head_euler(g, w, head_mod, g_in, x, dsigma, il, ws, ws_bytes, stream, nullptr);
   })());
 }
 

@@ -22,6 +22,10 @@
 // 16 x 64 partial products and moments of g - K in LDS; after one barrier every thread
 // combines two outputs of one token, adds shw + b and applies the Euler update to the
 // two latent values they land on.  LDS is double-buffered, so one barrier per tile.
+//
+// On a reuse step the head input is g = h_in + r (Eq. 1 with the cached r_j): the
+// kResid variant reads h_in and the bf16 residual cache and forms g in registers with
+// the same fp32 addition as the cache-apply kernel, so g never goes through HBM.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -54,7 +58,9 @@ __device__ inline size_t latent_index(const HeadGeo& hg, int m, int n) {
 // chunk j of wave w: chunks [cb, cb + kc) of the nch chunks of d
 __device__ inline int chunk_begin(int w, int nch) { return (w * nch) / kWaves; }
 
+template <bool kResid>
 __global__ void __launch_bounds__(512) k_head_euler_bf16(const float* __restrict__ gin,
+                                                         const uint16_t* __restrict__ resid,
                                                          const uint16_t* __restrict__ W,
                                                          const float* __restrict__ bias,
                                                          const float* __restrict__ shift,
@@ -91,16 +97,25 @@ __global__ void __launch_bounds__(512) k_head_euler_bf16(const float* __restrict
   // re-read lines already fetched, and every load stays unconditional, so the
   // compiler's wait counts do not fall back to waiting for everything at branch joins.)
   float4 ga[kRing][2];
-  auto load_chunk = [&](int t, int j, float4 (&dst)[2]) {
+  uint2 gr[kRing][2];                           // residual (bf16) of the same elements
+  auto load_chunk = [&](int t, int j, float4 (&dst)[2], uint2 (&rdst)[2]) {
     const int m = min(r0 + 16 * min(t, ntile - 1) + c16, r1 - 1);
-    const float* src = gin + size_t(m) * d + 32 * (cb + min(j, kc - 1)) + 4 * g4;
-    dst[0] = ld4(src);
-    dst[1] = ld4(src + 16);
+    const size_t e = size_t(m) * d + 32 * (cb + min(j, kc - 1)) + 4 * g4;
+    dst[0] = ld4(gin + e);
+    dst[1] = ld4(gin + e + 16);
+    if constexpr (kResid) {
+      rdst[0] = *reinterpret_cast<const uint2*>(resid + e);
+      rdst[1] = *reinterpret_cast<const uint2*>(resid + e + 16);
+    }
   };
-  auto load_k = [&](int t) { return gin[size_t(min(r0 + 16 * min(t, ntile - 1) + c16, r1 - 1)) * d]; };
+  auto load_k = [&](int t) {
+    const size_t e = size_t(min(r0 + 16 * min(t, ntile - 1) + c16, r1 - 1)) * d;
+    if constexpr (kResid) return gin[e] + __uint_as_float(uint32_t(resid[e]) << 16);
+    return gin[e];
+  };
   float kcur = load_k(0), knext = 0.f;
 #pragma unroll
-  for (int q = 0; q < kRing; ++q) load_chunk(0, q, ga[q]);
+  for (int q = 0; q < kRing; ++q) load_chunk(0, q, ga[q], gr[q]);
   // scale and shift (k = tid + 512 i), written to LDS once the slabs are done
   float scv[kChunks * kWaves * 32 / 512], shv[kChunks * kWaves * 32 / 512];
 #pragma unroll
@@ -234,7 +249,16 @@ __global__ void __launch_bounds__(512) k_head_euler_bf16(const float* __restrict
     for (int j = 0; j < kChunks; ++j) {
       if (j < kc) {
         const float4* v = ga[j % kRing];
-        const float e[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
+        float e[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
+        if constexpr (kResid) {                 // g = h_in + r, the cache-apply addition
+          const uint2* r = gr[j % kRing];
+          const uint32_t rw[4] = {r[0].x, r[0].y, r[1].x, r[1].y};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            e[2 * i] += __uint_as_float(rw[i] << 16);
+            e[2 * i + 1] += __uint_as_float(rw[i] & 0xFFFF0000u);
+          }
+        }
         const int k0 = 32 * (cb + j) + 4 * g4;
         const float4 sa = *reinterpret_cast<const float4*>(s_sc1 + k0);
         const float4 sb = *reinterpret_cast<const float4*>(s_sc1 + k0 + 16);
@@ -258,10 +282,10 @@ __global__ void __launch_bounds__(512) k_head_euler_bf16(const float* __restrict
       }
       // refill this slot with the chunk four ahead in the 8-chunk order of the tiles
       if (j + kRing < kChunks) {
-        load_chunk(t, j + kRing, ga[j % kRing]);
+        load_chunk(t, j + kRing, ga[j % kRing], gr[j % kRing]);
       } else {
         if (j == kChunks - kRing) knext = load_k(t + 1);
-        load_chunk(t + 1, j + kRing - kChunks, ga[j % kRing]);
+        load_chunk(t + 1, j + kRing - kChunks, ga[j % kRing], gr[j % kRing]);
       }
     }
 
@@ -320,15 +344,20 @@ bool head_euler_fused_ok(const Geo& g) {
   return g.bf16 && g.P == 64 && g.d % 32 == 0 && g.d >= 32 * kWaves && g.d <= 32 * kWaves * kChunks;
 }
 
-Status head_euler_bf16(const float* gin, const uint16_t* W, const float* bias, const float* shift,
-                       const float* scale, float* x, float dsigma, const Geo& g, hipStream_t s) {
+Status head_euler_bf16(const float* gin, const uint16_t* resid, const uint16_t* W, const float* bias,
+                       const float* shift, const float* scale, float* x, float dsigma, const Geo& g,
+                       hipStream_t s) {
   if (g.Nv <= 0) return Status::ok();
   if (!head_euler_fused_ok(g)) return Status::shape("fused bf16 head needs 64 outputs, d % 32 == 0 and 256 <= d <= 2048");
   const int grid = head_grid(g.Nv);
   if (grid <= 0) return Status::make(DC_ERR_HIP, "fused bf16 head: no device");
   const HeadGeo hg{g.T, g.Hl, g.Wl, g.p, g.Hp, g.Wp};
-  hipLaunchKernelGGL(k_head_euler_bf16, dim3(grid), dim3(512), 0, s, gin, W, bias, shift, scale, x,
-                     dsigma, g.Nv, g.d, g.eps, hg);
+  if (resid)
+    hipLaunchKernelGGL(k_head_euler_bf16<true>, dim3(grid), dim3(512), 0, s, gin, resid, W, bias, shift,
+                       scale, x, dsigma, g.Nv, g.d, g.eps, hg);
+  else
+    hipLaunchKernelGGL(k_head_euler_bf16<false>, dim3(grid), dim3(512), 0, s, gin, resid, W, bias, shift,
+                       scale, x, dsigma, g.Nv, g.d, g.eps, hg);
   DC_HIP(hipGetLastError());
   return Status::ok();
 }

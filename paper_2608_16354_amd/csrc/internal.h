@@ -137,10 +137,12 @@ Status gemm_bf16_head(const uint16_t* A, int lda, const uint16_t* W, const float
                       float dsigma, const Geo& g, int M, hipStream_t s);
 // bf16 model: LN-modulation + head projection + unpatchify + Euler update of one sample's
 // latent in one pass over its N_v video rows of g (head.hip); head_euler_fused_ok says
-// whether the shape is supported (64 outputs, d % 32 == 0, 256 <= d <= 2048).
+// whether the shape is supported (64 outputs, d % 32 == 0, 256 <= d <= 2048).  With
+// resid != NULL the input is g = gin + resid (bf16), formed in registers (reuse steps).
 bool head_euler_fused_ok(const Geo& g);
-Status head_euler_bf16(const float* gin, const uint16_t* W, const float* bias, const float* shift,
-                       const float* scale, float* x, float dsigma, const Geo& g, hipStream_t s);
+Status head_euler_bf16(const float* gin, const uint16_t* resid, const uint16_t* W, const float* bias,
+                       const float* shift, const float* scale, float* x, float dsigma, const Geo& g,
+                       hipStream_t s);
 
 // Attention over one sample: qk [M, 2d] (Q | K), vt [heads][Dh][ldv], out [M, d].
 // part: scratch for the split tail items (unnormalised partial outputs), part_bytes its size;

@@ -10,8 +10,9 @@
 //   3. scenes that refresh (planned, first step, or vetoed): snapshot u_j := u_k,
 //      h := h_in, run the L blocks, store r = h - h_in; vetoed scenes replan the
 //      unexecuted suffix from age zero with budget tau - C;
-//   4. scenes that reuse: h[:N_v] := h_in[:N_v] + r;
-//   5. head and Euler update from h[:N_v] for every scene.
+//   4. scenes that reuse: g = h_in[:N_v] + r (inside the fused bf16 head; otherwise
+//      written to h[:N_v] by the cache-apply kernel);
+//   5. head and Euler update from g (reuse) or h[:N_v] (refresh) for every scene.
 #include <cmath>
 #include <cstring>
 #include <limits>
@@ -30,7 +31,7 @@ Status block_forward(const Geo& g, const dc_block_weights* bw, const float* mod,
                      const IdxList& il, void* ws, size_t ws_bytes, hipStream_t s);
 Status head_euler(const Geo& g, const dc_model_weights* w, const float* head_mod, const float* gin,
                   float* x, float dsigma, const IdxList& il, void* ws, size_t ws_bytes,
-                  hipStream_t s);
+                  hipStream_t s, const void* resid);
 Status drift_call(const Geo& g, const float* h_in, const float* mod0, void* u_ref, int snapshot,
                   double* sums, const IdxList& il, void* ws, size_t ws_bytes, hipStream_t s);
 dc_status fail(const Status& s);
@@ -244,7 +245,10 @@ Status step(dc_sampler* s, int k, hipStream_t st, uint8_t* realized, double* dri
       DC_TRY(cache_store(bf.h, bf.h_in, bf.resid, ilb, g, st));
     }
   }
-  if (!reuse.empty()) {
+  // reuse scenes: the fused bf16 head reads h_in and r itself; other models apply the
+  // cache into h first
+  const bool fused_reuse = head_euler_fused_ok(g);
+  if (!reuse.empty() && !fused_reuse) {
     IdxList il;
     const std::vector<int32_t> rb = with_branches(reuse);
     DC_TRY(make_idx(rb.data(), int(rb.size()), il));
@@ -255,11 +259,26 @@ Status step(dc_sampler* s, int k, hipStream_t st, uint8_t* realized, double* dri
   // linear in v, so each branch's head adds its share
   const double dsig = s->sigmas[size_t(k)] - s->sigmas[size_t(k - 1)];
   const float* head_mod = mod_k + size_t(g.L) * 6 * g.d;
-  DC_TRY(head_euler(g, W, head_mod, bf.h, bf.x, float(s->cfg_on ? dsig * s->guidance : dsig), all,
-                    bf.ws, bf.ws_bytes, st));
-  if (s->cfg_on)
-    DC_TRY(head_euler(g, W, head_mod, bf.h + size_t(B) * row_stride, bf.x,
-                      float(dsig * (1.0 - double(s->guidance))), all, bf.ws, bf.ws_bytes, st));
+  const size_t rstride = size_t(g.Nv) * g.d * g.esz;      // one entry of the residual cache
+  const float dsig_c = float(s->cfg_on ? dsig * s->guidance : dsig);
+  const float dsig_u = float(dsig * (1.0 - double(s->guidance)));
+  const std::vector<int32_t>& from_h = fused_reuse ? refresh : ids;
+  if (!from_h.empty()) {
+    IdxList il;
+    DC_TRY(make_idx(from_h.data(), int(from_h.size()), il));
+    DC_TRY(head_euler(g, W, head_mod, bf.h, bf.x, dsig_c, il, bf.ws, bf.ws_bytes, st, nullptr));
+    if (s->cfg_on)
+      DC_TRY(head_euler(g, W, head_mod, bf.h + size_t(B) * row_stride, bf.x, dsig_u, il, bf.ws,
+                        bf.ws_bytes, st, nullptr));
+  }
+  if (fused_reuse && !reuse.empty()) {
+    IdxList il;
+    DC_TRY(make_idx(reuse.data(), int(reuse.size()), il));
+    DC_TRY(head_euler(g, W, head_mod, bf.h_in, bf.x, dsig_c, il, bf.ws, bf.ws_bytes, st, bf.resid));
+    if (s->cfg_on)
+      DC_TRY(head_euler(g, W, head_mod, bf.h_in + size_t(B) * row_stride, bf.x, dsig_u, il, bf.ws,
+                        bf.ws_bytes, st, static_cast<const char*>(bf.resid) + size_t(B) * rstride));
+  }
 
   // controller state
   for (int b = 0; b < B; ++b) {

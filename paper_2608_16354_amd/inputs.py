@@ -11,6 +11,8 @@ does not depend on how many threads draw it.
 """
 from __future__ import annotations
 
+import hashlib
+import json
 import math
 import os
 from concurrent.futures import ThreadPoolExecutor
@@ -373,3 +375,26 @@ def scene_problem(w: Workload, m: Motion, tau_q: int = TAU_INF, thr: float | Non
     legal = np.ones(w.K, np.uint8)
     return SchedProblem(w.K, w.h_max, w.cap, legal, None, xy, yaw, L0, Th0, L1, Th1, w.eps,
                         q0, q1, d0, d1, tau_q)
+
+
+# ----------------------------------------------------------------------------
+# fingerprints (run records and stored oracle samples)
+# ----------------------------------------------------------------------------
+def input_fingerprint(w: Workload) -> str:
+    """sha256 over a few generated tensors (scene 0's latent and text, the patch
+    embedding, the head, slices of the first and last block): a changed generator
+    changes it."""
+    W = Weights(w.model, w.cfg_id)
+    h = hashlib.sha256()
+    for a in (latent(w.model, w.cfg_id, 0), text(w.model, w.cfg_id, 0), W.get("w_pe"),
+              W.get("w_head"), W.block(0, "w_qkv")[:64], W.block(w.model.n_blocks - 1, "w_2")[:64]):
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h.hexdigest()
+
+
+def config_hash(w: Workload, tau_q: int, input_fp: str) -> str:
+    """sha256 of the workload definition (shape, schedule parameters, scene motions),
+    the budget and the input fingerprint: one value per run configuration."""
+    rec = {"workload": repr(w), "motions": [repr(m) for m in scene_motions(w)],
+           "tau_q": int(tau_q), "inputs": input_fp}
+    return hashlib.sha256(json.dumps(rec, sort_keys=True).encode()).hexdigest()

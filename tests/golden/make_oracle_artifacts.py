@@ -14,7 +14,6 @@ charge, the budget tau and a fingerprint of the generated inputs.  With
 truncated artefact at every point).
 """
 import argparse
-import hashlib
 import os
 import sys
 import time
@@ -30,14 +29,7 @@ from paper_2608_16354_amd import inputs as I  # noqa: E402
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def fingerprint(w):
-    """Hash of the generated inputs, so a changed generator is detected."""
-    W = I.Weights(w.model, w.cfg_id)
-    h = hashlib.sha256()
-    for a in (I.latent(w.model, w.cfg_id, 0), I.text(w.model, w.cfg_id, 0), W.get("w_pe"),
-              W.get("w_head"), W.block(0, "w_qkv")[:64], W.block(w.model.n_blocks - 1, "w_2")[:64]):
-        h.update(np.ascontiguousarray(a).tobytes())
-    return h.hexdigest()
+fingerprint = I.input_fingerprint      # hash of the generated inputs (a changed generator is detected)
 
 
 def artefact_path(name, tag=None):
