@@ -157,6 +157,18 @@ dc_status dc_drift_l1(const dc_model_cfg* cfg, const float* h_in, const float* m
                       void* u_ref, int32_t snapshot, double* sums, const int32_t* idx,
                       int32_t n, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* dc_drift_l1 for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same computation
+ * and results, bit for bit, without a workspace argument.  The partial sums of the
+ * reduction live in a fixed device array inside the library, one copy per GPU
+ * (2 MiB, held until the process ends; its address is looked up on the first call on
+ * each device).  Limit: n <= DC_MAX_BATCH samples (DC_ERR_ARG beyond); any model shape
+ * dc_drift_l1 takes.  The call allocates nothing.  Calls that overlap on one GPU
+ * (several streams or threads at once) share the array and race: serialise them. */
+dc_status dc_drift_l1_noalloc(const dc_model_cfg* cfg, const float* h_in, const float* mod0,
+                              void* u_ref, int32_t snapshot, double* sums, const int32_t* idx,
+                              int32_t n, hipStream_t stream);
+
 /* Output interface H_k and the sampler update (Eq. 1): y = LN(g)(1+scale_f)+shift_f
  * on the video rows of g (f32 [B, N, d]), v = unpatchify(y w_head^T + b_head),
  * x[b] += dsigma * v.  head_mod: f32 [2, d] (shift_f, scale_f); x: f32 [B, C, T, H, W].

@@ -78,6 +78,7 @@ SIGNATURES = {
     "dc_cache_apply": (C.c_int32, [P(ModelCfg), vp, vp, vp, i32p, C.c_int32, vp]),
     "dc_drift_l1": (C.c_int32, [P(ModelCfg), vp, vp, vp, C.c_int32, vp, i32p, C.c_int32, vp,
                                 C.c_size_t, vp]),
+    "dc_drift_l1_noalloc": (C.c_int32, [P(ModelCfg), vp, vp, vp, C.c_int32, vp, i32p, C.c_int32, vp]),
     "dc_head_euler": (C.c_int32, [P(ModelCfg), P(ModelWeights), vp, vp, vp, C.c_float, i32p,
                                   C.c_int32, vp, C.c_size_t, vp]),
     "dc_schedule_dp": (C.c_int32, [P(SchedProblem), P(Schedule)]),

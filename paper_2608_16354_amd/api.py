@@ -143,6 +143,14 @@ def dc_drift_l1(cfg, h_in, mod0, u_ref, snapshot, sums, idx, ws: Workspace, stre
         ws.ptr, ws.nbytes, _stream(stream)))
 
 
+def dc_drift_l1_noalloc(cfg, h_in, mod0, u_ref, snapshot, sums, idx, stream=None):
+    """dc_drift_l1 without a workspace (the library's fixed per-GPU scratch)."""
+    arr, p, n = _idx(idx)
+    L.check("dc_drift_l1_noalloc", L.load().dc_drift_l1_noalloc(
+        C.byref(cfg), _ptr(h_in), _ptr(mod0), _ptr(u_ref), int(bool(snapshot)), _ptr(sums), p, n,
+        _stream(stream)))
+
+
 def dc_head_euler(dm: DeviceModel, head_mod, g, x, dsigma, idx, ws: Workspace, stream=None):
     arr, p, n = _idx(idx)
     L.check("dc_head_euler", L.load().dc_head_euler(

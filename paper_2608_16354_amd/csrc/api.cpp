@@ -358,6 +358,20 @@ dc_status dc_drift_l1(const dc_model_cfg* cfg, const float* h_in, const float* m
   })());
 }
 
+dc_status dc_drift_l1_noalloc(const dc_model_cfg* cfg, const float* h_in, const float* mod0,
+                              void* u_ref, int32_t snapshot, double* sums, const int32_t* idx,
+                              int32_t n, hipStream_t stream) {
+  DC_ENTRY(([&]() -> Status {
+    Geo g;
+    IdxList il;
+    DC_TRY(make_geo(cfg, g));
+    DC_TRY(make_idx(idx, n, il));
+    if (!h_in || !mod0 || !u_ref || (!snapshot && !sums)) return Status::arg("NULL argument");
+    if (il.n == 0) return Status::ok();
+    return drift_noalloc(h_in, mod0, u_ref, snapshot != 0, sums, il, g, stream);
+  })());
+}
+
 dc_status dc_head_euler(const dc_model_cfg* cfg, const dc_model_weights* w, const float* head_mod,
                         const float* g_in, float* x, float dsigma, const int32_t* idx, int32_t n,
                         void* ws, size_t ws_bytes, hipStream_t stream) {

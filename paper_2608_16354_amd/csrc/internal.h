@@ -161,6 +161,9 @@ Status cache_apply(const float* h_in, const void* resid, float* gout, const IdxL
                    const Geo& g, hipStream_t s);
 Status drift(const float* h_in, const float* mod0, void* u_ref, bool snapshot, double* sums,
              const IdxList& idx, const Geo& g, double* part, hipStream_t s);
+// drift() with the partial sums in the library's fixed per-GPU scratch array (no workspace)
+Status drift_noalloc(const float* h_in, const float* mod0, void* u_ref, bool snapshot, double* sums,
+                     const IdxList& idx, const Geo& g, hipStream_t s);
 Status patchify(const float* x, float* patches, const Geo& g, hipStream_t s);
 Status copy_text(const float* txt, float* h_in, const Geo& g, hipStream_t s);
 Status copy_rows(const float* src, float* dst, size_t count, hipStream_t s);

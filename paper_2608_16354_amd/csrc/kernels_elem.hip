@@ -4,7 +4,9 @@
 // vector accesses.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include "internal.h"
 
@@ -421,6 +423,48 @@ Status assemble_modulation(const float* m, const float* c, const float* offset, 
                      c, offset, L, l, g.d, mod, k0);
   DC_LAUNCH_CHECK();
   return Status::ok();
+}
+
+// ---------------------------------------------------------------------------
+// Drift without a workspace (for callers that cannot allocate): the per-block
+// partial sums live in a fixed device array, one copy per GPU, held until the
+// process ends.  Capacity: DC_MAX_BATCH samples x kDriftBlocks blocks x 4 sums
+// (2 MiB); every partial the second pass reads is written by the same call, so
+// nothing needs clearing.  Calls that overlap on one GPU share the array and race.
+// ---------------------------------------------------------------------------
+constexpr size_t kDriftScratchDoubles = size_t(DC_MAX_BATCH) * kDriftBlocks * 4;
+static __device__ __align__(256) double scratch[kDriftScratchDoubles];
+
+namespace {
+// Device address of this GPU's copy of `scratch` (host code must not use the
+// symbol's name as a pointer), looked up once per device with that device current.
+Status scratch_address(double** out) {
+  static std::mutex mu;
+  static std::vector<double*> per_device;
+  int dev = 0;
+  DC_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lock(mu);
+  if (size_t(dev) >= per_device.size()) per_device.resize(size_t(dev) + 1, nullptr);
+  if (!per_device[size_t(dev)]) {
+    void* p = nullptr;
+    DC_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return Status::make(DC_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    per_device[size_t(dev)] = static_cast<double*>(p);
+  }
+  *out = per_device[size_t(dev)];
+  return Status::ok();
+}
+}  // namespace
+
+Status drift_noalloc(const float* h_in, const float* mod0, void* u_ref, bool snapshot, double* sums,
+                     const IdxList& idx, const Geo& g, hipStream_t s) {
+  const size_t nblk = size_t(std::min(kDriftBlocks, (g.Nv + 3) / 4));
+  if (size_t(idx.n) * nblk * 4 > kDriftScratchDoubles)
+    return Status::arg("dc_drift_l1_noalloc: more samples than its fixed scratch holds (" +
+                       std::to_string(DC_MAX_BATCH) + ")");
+  double* part = nullptr;
+  DC_TRY(scratch_address(&part));
+  return drift(h_in, mod0, u_ref, snapshot, sums, idx, g, part, s);
 }
 
 }  // namespace dc
