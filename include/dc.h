@@ -245,6 +245,32 @@ dc_status dc_select_anchors(const double* L, const double* Theta, int32_t n, dou
                             double* anchors, int32_t* index);
 
 /* ---------------------------------------------------------------------------
+ * Anchor calibration of the run tables (Sec. 3.1 after Eq. 4; Eq. 5-7).
+ * ------------------------------------------------------------------------- */
+
+/* Bytes of device workspace dc_calibrate_tables needs for K steps (the full trace of
+ * x_k, u_k, r_k plus the tangent-mode activations of one network pass). */
+size_t dc_calibrate_workspace_bytes(const dc_model_cfg* cfg, int32_t K);
+
+/* The response and drift tables of one anchor clip, from its full (uncached) denoising
+ * trace: for a run refreshed at step j and reused for h steps (row j-1, column h-1),
+ *   d[j,h] = ||u_{j+h} - u_j||_2 / (||u_{j+h}||_2 + eps)                      (Eq. 5)
+ *   e_{j,l} = H_{j+l}(x_{j+l}, r_j) - H_{j+l}(x_{j+l}, r_{j+l})               (Eq. 6)
+ *   q[j,h] = ||sum_{l<=h} P_{j+l} e_{j,l}||_2 / (||x_out||_2 + eps)            (Eq. 7)
+ * where u, r, x are the trace's backbone inputs, backbone outputs and latents, H_k(x, r)
+ * the head's denoiser output for g = h_in(x)[video] + r, x_out the terminal latent, and
+ * P_t e the terminal-latent tangent when the denoiser output of step t moves by e (a
+ * Jacobian-vector product of the network at every later step of the trace).  Entries
+ * with j + h > K are 0.  x1: device f32 [C, T, H, W] (the clip's initial noise); txt:
+ * device f32 [N_t, d]; sigmas: host f64 [K+1]; q, d: host f64 [(K-1), h_max] out, the
+ * q0/d0 (or q1/d1) of dc_sched_problem.  fp32 models only (DC_ERR_DTYPE otherwise);
+ * head_dim 64.  Waits on `stream` (the table entries are read back). */
+dc_status dc_calibrate_tables(const dc_model_cfg* cfg, const dc_model_weights* w, const float* x1,
+                              const float* txt, const double* sigmas, int32_t K, int32_t h_max,
+                              double eps, double* q, double* d, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Sampler: the causal controller of Sec. 3.2 around the device steps.
  * ------------------------------------------------------------------------- */
 typedef struct dc_sampler dc_sampler;

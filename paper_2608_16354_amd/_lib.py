@@ -81,6 +81,10 @@ SIGNATURES = {
     "dc_drift_l1_noalloc": (C.c_int32, [P(ModelCfg), vp, vp, vp, C.c_int32, vp, i32p, C.c_int32, vp]),
     "dc_head_euler": (C.c_int32, [P(ModelCfg), P(ModelWeights), vp, vp, vp, C.c_float, i32p,
                                   C.c_int32, vp, C.c_size_t, vp]),
+    "dc_calibrate_workspace_bytes": (C.c_size_t, [P(ModelCfg), C.c_int32]),
+    "dc_calibrate_tables": (C.c_int32, [P(ModelCfg), P(ModelWeights), vp, vp, P(C.c_double), C.c_int32,
+                                        C.c_int32, C.c_double, P(C.c_double), P(C.c_double), vp,
+                                        C.c_size_t, vp]),
     "dc_schedule_dp": (C.c_int32, [P(SchedProblem), P(Schedule)]),
     "dc_select_tau": (C.c_int32, [P(SchedProblem), C.c_int32, C.c_double, P(C.c_int64)]),
     "dc_motion_statistics": (C.c_int32, [P(C.c_double), P(C.c_double), C.c_int32, P(C.c_double),

@@ -158,6 +158,29 @@ def dc_head_euler(dm: DeviceModel, head_mod, g, x, dsigma, idx, ws: Workspace, s
         ws.ptr, ws.nbytes, _stream(stream)))
 
 
+def dc_calibrate_tables(dm: DeviceModel, x1, txt, sigmas, h_max: int, eps: float, stream=None):
+    """Anchor calibration of one clip (Eq. 5-7) on the GPU: returns (q, d), f64
+    [(K-1), h_max] each.  x1 [C, T, H, W], txt [N_t, d]: the clip's inputs (torch
+    tensors on the device); sigmas: the K+1 noise levels."""
+    torch = _torch()
+    sig = np.ascontiguousarray(np.asarray(sigmas, np.float64))
+    K = sig.size - 1
+    nbytes = L.load().dc_calibrate_workspace_bytes(C.byref(dm.cfg), K)
+    if nbytes == 0:
+        raise L.DriveCacheError("dc_calibrate_workspace_bytes", L.DC_ERR_ARG, "bad model or K")
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dm.device)
+    q = np.zeros((K - 1, h_max), np.float64)
+    d = np.zeros((K - 1, h_max), np.float64)
+    x1 = x1.to(device=dm.device, dtype=torch.float32).contiguous()
+    txt = txt.to(device=dm.device, dtype=torch.float32).contiguous()
+    L.check("dc_calibrate_tables", L.load().dc_calibrate_tables(
+        C.byref(dm.cfg), C.byref(dm.cweights), _ptr(x1), _ptr(txt),
+        sig.ctypes.data_as(C.POINTER(C.c_double)), K, int(h_max), float(eps),
+        q.ctypes.data_as(C.POINTER(C.c_double)), d.ctypes.data_as(C.POINTER(C.c_double)),
+        int(ws.data_ptr()), nbytes, _stream(stream)))
+    return q, d
+
+
 class _CProblem:
     """A dc_sched_problem whose arrays stay alive with it."""
 

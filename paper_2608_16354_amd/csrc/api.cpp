@@ -384,6 +384,23 @@ dc_status dc_head_euler(const dc_model_cfg* cfg, const dc_model_weights* w, cons
   })());
 }
 
+size_t dc_calibrate_workspace_bytes(const dc_model_cfg* cfg, int32_t K) {
+  Geo g;
+  if (!make_geo(cfg, g) || K < 1) return 0;
+  return calibrate_workspace_bytes(g, K);
+}
+
+dc_status dc_calibrate_tables(const dc_model_cfg* cfg, const dc_model_weights* w, const float* x1,
+                              const float* txt, const double* sigmas, int32_t K, int32_t h_max,
+                              double eps, double* q, double* d, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  DC_ENTRY(([&]() -> Status {
+    Geo g;
+    DC_TRY(make_geo(cfg, g));
+    return calibrate_tables(g, w, x1, txt, sigmas, K, h_max, eps, q, d, ws, ws_bytes, stream);
+  })());
+}
+
 dc_status dc_schedule_dp(const dc_sched_problem* p, dc_schedule* out) {
   DC_ENTRY(([&]() -> Status {
     if (!p || !out || !out->reuse) return Status::arg("NULL argument");

@@ -165,6 +165,25 @@ Status drift(const float* h_in, const float* mod0, void* u_ref, bool snapshot, d
 Status drift_noalloc(const float* h_in, const float* mod0, void* u_ref, bool snapshot, double* sums,
                      const IdxList& idx, const Geo& g, hipStream_t s);
 Status patchify(const float* x, float* patches, const Geo& g, hipStream_t s);
+
+// Anchor calibration (Eq. 5-7): tangent-mode kernels of the fp32 network (calib.hip) and
+// the driver (calib.cpp).  a = LN(x)(1+scale)+shift and da its tangent along dx, per row;
+// o, dout = attention over qkv [M, 3d] and its tangent along dqkv; z, dz <- GELU(z) and
+// its tangent; out = alpha x + beta y (y may be NULL); sumsq -> out2 = (sum (a-b)^2, sum a^2)
+// (b may be NULL) in a fixed order, with sumsq_scratch_doubles() doubles of scratch.
+Status ln_mod_jvp(const float* x, const float* dx, int rows, int ld, int d, const float* shift,
+                  const float* scale, float* a, float* da, float eps, hipStream_t s);
+Status attention_jvp_f32(const float* qkv, const float* dqkv, const Geo& g, int M, float* o,
+                         float* dout, hipStream_t s);
+Status gelu_jvp(float* z, float* dz, size_t n, hipStream_t s);
+Status lincomb(float* out, const float* x, float alpha, const float* y, float beta, size_t n,
+               hipStream_t s);
+size_t sumsq_scratch_doubles();
+Status sumsq(const float* a, const float* b, size_t n, double* scratch, double* out2, hipStream_t s);
+size_t calibrate_workspace_bytes(const Geo& g, int K);
+Status calibrate_tables(const Geo& g, const dc_model_weights* w, const float* x1, const float* txt,
+                        const double* sigmas, int K, int h_max, double eps, double* q, double* dtab,
+                        void* ws, size_t ws_bytes, hipStream_t s);
 Status copy_text(const float* txt, float* h_in, const Geo& g, hipStream_t s);
 Status copy_rows(const float* src, float* dst, size_t count, hipStream_t s);
 Status time_features(const double* sig, int K, float* e, int n_freq, hipStream_t s);

@@ -1,0 +1,87 @@
+"""Anchor calibration on the GPU (dc_calibrate_tables; Sec. 3.1 after Eq. 4, Eq. 5-7)
+against the oracle (oracle/calibrate.py) on the small fp32 workload, element by element,
+and the host DP on the resulting tables against the oracle's DP, bit for bit."""
+import numpy as np
+import pytest
+
+from oracle import calibrate as cal
+from oracle import dit, dp
+from paper_2608_16354_amd import inputs as I
+from tests.gpu_util import say
+
+pytestmark = pytest.mark.gpu
+
+W_TINY = I.WORKLOADS["dit-tiny-f32"]
+
+
+@pytest.fixture(scope="module")
+def api():
+    from paper_2608_16354_amd import api as A
+    A.L.load()
+    return A
+
+
+def _gpu_tables(api, dm, w, scene, dev):
+    import torch
+    m = w.model
+    x1 = torch.from_numpy(I.latent(m, w.cfg_id, scene)).to(dev)
+    txt = torch.from_numpy(I.text(m, w.cfg_id, scene)).to(dev)
+    return api.dc_calibrate_tables(dm, x1, txt, I.sigmas(w.K), w.h_max, w.eps)
+
+
+def _oracle_tables(W, w, scene):
+    P = dit.Params(W)
+    m = w.model
+    tr = cal.Trace(P, I.latent(m, w.cfg_id, scene).astype(np.float64),
+                   I.text(m, w.cfg_id, scene).astype(np.float64), I.sigmas(w.K))
+    return cal.run_tables(tr, w.h_max, w.eps)
+
+
+def test_calibrated_tables_match_oracle_and_plan_bit_exact(api, dev):
+    w = W_TINY
+    W = I.Weights(w.model, w.cfg_id)
+    dm = api.DeviceModel(W, dev)
+    tabs = []
+    for scene in (0, 1):                      # the two anchor clips
+        say("calibration, anchor clip", scene)
+        q, d = _gpu_tables(api, dm, w, scene, dev)
+        qo, do = _oracle_tables(W, w, scene)
+        assert np.array_equal(q == 0.0, qo == 0.0) and np.array_equal(d == 0.0, do == 0.0)
+        nz = qo != 0.0
+        eq = np.abs(q[nz] - qo[nz]) / qo[nz]
+        ed = np.abs(d[d != 0] - do[do != 0]) / do[do != 0]
+        say("anchor", scene, "q max rel err", float(eq.max()), "d max rel err", float(ed.max()),
+            "q range", float(qo[nz].min()), float(qo[nz].max()))
+        assert eq.max() < 1e-5                # measured 9e-7 (fp32 tangents vs the fp64 oracle)
+        assert ed.max() < 1e-6                # measured 9e-8
+        tabs.append((q, d))
+    (q0, d0), (q1, d1) = tabs
+    # the planner on the GPU tables: the library's schedule equals the oracle's bit for bit
+    for mo in (w.motions[0], I.Motion(2.0, 0.0), I.Motion(9.0, 0.2)):
+        p = I.scene_problem(w, mo).replace(q0=q0, q1=q1, d0=d0, d1=d1)
+        plan = dp.schedule(p)
+        a = api.dc_schedule_dp(p)
+        assert a.reuse == plan.reuse and (a.n_reuse, a.cost_q) == (plan.n_reuse, plan.cost_q)
+        assert a.chat_q.tolist() == plan.tables.chat_q
+
+
+def test_zero_residual_gives_zero_responses(api, dev):
+    """Zero output projections make every cached residual zero: each perturbation of
+    Eq. 6 vanishes exactly, so every response of Eq. 7 is exactly 0 while the inputs
+    still drift (Eq. 5)."""
+    w = W_TINY
+    Wz = I.Weights(w.model, w.cfg_id, zero_out=("w_o", "b_o", "w_2", "b_2"))
+    dm = api.DeviceModel(Wz, dev)
+    say("calibration, zero residual")
+    q, d = _gpu_tables(api, dm, w, 0, dev)
+    assert np.all(q == 0.0)
+    assert np.all(d[:-1] > 0.0)
+
+
+def test_bf16_model_is_refused(api, dev):
+    import dataclasses
+    w = dataclasses.replace(W_TINY, model=dataclasses.replace(W_TINY.model, dtype="bf16"))
+    W = I.Weights(w.model, w.cfg_id)
+    dm = api.DeviceModel(W, dev)
+    with pytest.raises(api.L.DriveCacheError):
+        _gpu_tables(api, dm, w, 0, dev)
