@@ -70,6 +70,7 @@ def hbm_bytes(m):
         "cache_store": Nv * d * (4 + 4 + e),                   # read h_out, h_in; write r
         "cache_apply": Nv * d * (4 + e + 4),                   # read h_in, r; write g
         "head": Nv * d * 4 + 2 * lat,                          # read g; read and write x
+        "head_reuse": Nv * d * (4 + e) + 2 * lat,              # read h_in and r; read and write x
         "ln_modulate": N * d * (4 + e),                        # read h; write a
     }
 
@@ -107,7 +108,7 @@ def host_info():
 
 def cpu_baseline(w, W, schedule, budget_s=30.0):
     """The fp64 oracle on a bounded sample of the same workload, extrapolated to one
-    cached sample: one block at full length on two query-row subsets (1024 and 4096 rows) (the per-block
+    cached sample: one block at full length on two query-row subsets (2048 and 8192 rows) (the per-block
     cost is fixed key/value work plus a per-row cost) and one full reuse step."""
     import numpy as np
     from oracle import dit
@@ -119,13 +120,13 @@ def cpu_baseline(w, W, schedule, budget_s=30.0):
     h = I.hidden_state(m, (90,)).astype(np.float64)
     rng = np.random.default_rng(0)
     times = {}
-    for R in (1024, 4096):
+    for R in (2048, 8192):
         rows = np.sort(rng.choice(m.n_tok, R, replace=False))
         t0 = time.perf_counter()
         dit.block(P, 0, mods[0], h, rows=rows)
         times[R] = time.perf_counter() - t0
-    per_row = (times[4096] - times[1024]) / (4096 - 1024)
-    fixed = max(times[1024] - 1024 * per_row, 0.0)
+    per_row = (times[8192] - times[2048]) / (8192 - 2048)
+    fixed = max(times[2048] - 2048 * per_row, 0.0)
     t_block = fixed + m.n_tok * per_row
     x = I.latent(m, w.cfg_id, 0).astype(np.float64)
     txt = I.text(m, w.cfg_id, 0)
@@ -144,8 +145,8 @@ def cpu_baseline(w, W, schedule, budget_s=30.0):
     cpu, blas = host_info()
     return {"value": w.batch * m.n_v * w.K / (w.batch * t_sample), "unit": "latent token*steps/s",
             "cores": cores, "kind": "oracle", "dtype": "f64", "cpu_model": cpu, "blas": blas,
-            "sample": (f"fp64 oracle: one block at {m.n_tok} tokens on 1024 and 4096 query rows "
-                       f"({times[1024]:.1f}s, {times[4096]:.1f}s) + one full reuse step ({t_reuse:.1f}s), "
+            "sample": (f"fp64 oracle: one block at {m.n_tok} tokens on 2048 and 8192 query rows "
+                       f"({times[2048]:.1f}s, {times[8192]:.1f}s) + one full reuse step ({t_reuse:.1f}s), "
                        f"extrapolated to the {n_ref}-refresh/{n_reu}-reuse schedule; {spent:.0f}s of CPU work")}
 
 

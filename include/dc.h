@@ -346,7 +346,8 @@ void dc_sampler_destroy(dc_sampler* s);
  * Kernel timing (a measurement aid; off by default).
  * Classes: 0 attention, 1 QKV GEMM, 2 output-projection GEMM, 3 MLP-up GEMM,
  * 4 MLP-down GEMM, 5 AdaLN modulation, 6 patch embedding, 7 drift reduction,
- * 8 cache store, 9 cache apply, 10 head + Euler.
+ * 8 cache store, 9 cache apply, 10 head + Euler, 11 head + Euler on a reuse step of a
+ * bf16 model (its input g = h_in + r formed in the kernel).
  * ------------------------------------------------------------------------- */
 
 /* Bit c of mask enables timing of class c: each launch is bracketed by two

@@ -104,7 +104,7 @@ SIGNATURES = {
 }
 
 KERNEL_CLASSES = ("attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "ln_modulate",
-                  "patch_embed", "drift", "cache_store", "cache_apply", "head")
+                  "patch_embed", "drift", "cache_store", "cache_apply", "head", "head_reuse")
 
 _lib = None
 

@@ -234,7 +234,7 @@ Status head_euler(const Geo& g, const dc_model_weights* w, const float* head_mod
   for (int i = 0; i < il.n; ++i) {
     const int b = il.v[i];
     const float* gb = gin + size_t(b) * g.N * g.d;
-    ProfScope ps(KClass::kHead, s);
+    ProfScope ps(resid ? KClass::kHeadReuse : KClass::kHead, s);
     if (head_euler_fused_ok(g)) {
       const uint16_t* rb = resid ? static_cast<const uint16_t*>(resid) + size_t(b) * g.Nv * g.d : nullptr;
       DC_TRY(head_euler_bf16(gb, rb, static_cast<const uint16_t*>(w->w_head), w->b_head, head_mod,

@@ -69,7 +69,7 @@ Status make_geo(const dc_model_cfg* cfg, Geo& g);
 
 // Kernel classes that can be timed (dc_profile_*); the numbering is part of the ABI.
 enum class KClass { kAttention = 0, kGemmQKV, kGemmOut, kGemmUp, kGemmDown, kLnModulate,
-                    kPatchEmbed, kDrift, kCacheStore, kCacheApply, kHead, kCount };
+                    kPatchEmbed, kDrift, kCacheStore, kCacheApply, kHead, kHeadReuse, kCount };
 
 // RAII: brackets the launches made in its scope with events when the class is enabled.
 class ProfScope {
