@@ -161,7 +161,7 @@ def run_record(api, w, probs, realized, drift, plans):
         j, age, checks = 1, 0, []
         for k in range(1, w.K + 1):
             d = float(drift[k - 1, b])
-            if not np.isnan(d):
+            if not np.isnan(d) and age < dbar.shape[1]:
                 thr = float(dbar[j - 1, age])
                 checks.append({"k": k, "drift": d, "threshold": thr, "margin": thr - d})
             if realized[k - 1, b]:
