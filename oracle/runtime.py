@@ -79,7 +79,8 @@ def drift_value(sums, eps, metric="l1"):
 
 
 def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
-           W_low=None, k_switch=None, guidance=None, txt_null=None, steps=None, on_step=None):
+           W_low=None, k_switch=None, guidance=None, txt_null=None, steps=None, on_step=None,
+           resume=None):
     """One cached K-step sample of one scene.
 
     W: `Weights`; x1 [C,T,H,W]; txt [n_txt, d]; sigmas [K+1]; prob: `SchedProblem`.
@@ -90,8 +91,11 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
     must change at k_switch).  guidance, txt_null: the guidance scale w and the
     unconditional text; the branches keep separate caches.
     steps: stop after this many steps (default K); the result then holds x_{steps+1}.
-    on_step(k, x, records, plan): called after each step with the latent x_{k+1}, the
-    records so far and the current plan (for writing intermediate results)."""
+    on_step(k, x, records, plan, state): called after each step with the latent x_{k+1},
+    the records so far, the current plan and the whole controller state (a dict), for
+    writing intermediate results.
+    resume: such a state dict; the sample continues after its step (a long run can be
+    stopped and picked up again without recomputing the executed steps)."""
     experts = [dit.Params(W)]
     if W_low is not None:
         if prob.segment is None or prob.segment[k_switch - 1] == prob.segment[k_switch - 2]:
@@ -113,7 +117,14 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
     r_u = None
     u_ref = None
     records = []
-    for k in range(1, (K if steps is None else min(steps, K)) + 1):
+    k0 = 1
+    if resume is not None:
+        x, mask, C, n_done, j, age = resume["x"], list(resume["mask"]), resume["C"], resume["n_done"], \
+            resume["j"], resume["age"]
+        r, r_u, u_ref = resume["r"], resume["r_u"], resume["u_ref"]
+        records, plans = list(resume["records"]), list(resume["plans"])
+        k0 = resume["k"] + 1
+    for k in range(k0, (K if steps is None else min(steps, K)) + 1):
         P = experts[1] if (W_low is not None and k >= k_switch) else experts[0]
         mods, head_mod = dit.step_modulation(P, sigmas[k - 1])
         h_in = dit.embed(P, x, txt)
@@ -162,5 +173,7 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
             v = v_u + guidance * (v - v_u)
         x = dit.euler(x, v, sigmas[k - 1], sigmas[k])
         if on_step is not None:
-            on_step(k, x, records, mask)
+            on_step(k, x, records, mask, {"k": k, "x": x, "mask": list(mask), "C": C, "n_done": n_done,
+                                          "j": j, "age": age, "r": r, "r_u": r_u, "u_ref": u_ref,
+                                          "records": list(records), "plans": list(plans)})
     return SampleResult(x, records, plans, C, mask)

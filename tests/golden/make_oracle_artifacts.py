@@ -3,7 +3,7 @@ Calls only the oracle and the seeded input generator.
 
     python tests/golden/make_oracle_artifacts.py dit-12x1152-bf16
     python tests/golden/make_oracle_artifacts.py dit-12x1152-bf16 --thr 0.05 --tag veto
-    python tests/golden/make_oracle_artifacts.py dit-30x1920-bf16 --every-step
+    python tests/golden/make_oracle_artifacts.py dit-30x1920-bf16 --every-step --checkpoint <file>
 
 The file `oracle_<workload>[-<tag>].npz` holds the latent after `steps` steps
 (float32), the realized, planned and vetoed flags of every step, every observed
@@ -11,10 +11,13 @@ drift (rel-L1 and rel-L2; NaN where no check ran) with the threshold it was
 compared with, the plan as it stood after the last step, the veto count, the
 charge, the budget tau and a fingerprint of the generated inputs.  With
 --every-step the file is rewritten after each step (a long run leaves a valid
-truncated artefact at every point).
+truncated artefact at every point); with --checkpoint the whole controller state is
+saved after each step to that file (this script's own pickle) and a run started
+with an existing checkpoint continues after its step.
 """
 import argparse
 import os
+import pickle
 import sys
 import time
 
@@ -67,6 +70,7 @@ def main(argv=None):
     ap.add_argument("--tag", default=None, help="suffix of the file name")
     ap.add_argument("--steps", type=int, default=None, help="stop after this many steps")
     ap.add_argument("--every-step", action="store_true", help="rewrite the file after every step")
+    ap.add_argument("--checkpoint", default=None, help="state file to save after each step and resume from")
     a = ap.parse_args(argv)
     w = I.WORKLOADS[a.name]
     thr = w.thr if a.thr is None else a.thr
@@ -78,8 +82,19 @@ def main(argv=None):
     path = artefact_path(a.name, a.tag)
     t0 = time.time()
 
-    def on_step(k, x, records, plan):
+    resume = None
+    if a.checkpoint and os.path.exists(a.checkpoint):
+        with open(a.checkpoint, "rb") as f:
+            resume = pickle.load(f)
+        print(f"{a.name}: resuming after step {resume['k']}", flush=True)
+
+    def on_step(k, x, records, plan, state):
         W.drop()          # the oracle keeps its own float64 copies of every tensor it used
+        if a.checkpoint:
+            tmp = a.checkpoint + ".tmp"
+            with open(tmp, "wb") as f:
+                pickle.dump(state, f, protocol=pickle.HIGHEST_PROTOCOL)
+            os.replace(tmp, a.checkpoint)
         r = records[-1]
         d = "" if r.drift is None else f" drift {r.drift:.6f} thr {r.threshold:.4f}"
         print(f"{a.name} step {k}: {'reuse' if r.realized else 'full'}{' (vetoed)' if r.vetoed else ''}"
@@ -88,7 +103,7 @@ def main(argv=None):
             _write(path, a.name, thr, tau, fp, k, x, records, plan, time.time() - t0)
 
     res = runtime.sample(W, I.latent(w.model, w.cfg_id, 0), I.text(w.model, w.cfg_id, 0),
-                         I.sigmas(w.K), p, steps=a.steps, on_step=on_step)
+                         I.sigmas(w.K), p, steps=a.steps, on_step=on_step, resume=resume)
     k = len(res.records)
     _write(path, a.name, thr, tau, fp, k, res.x, res.records, res.plan, time.time() - t0)
     print(f"{a.name}: {time.time() - t0:.1f} s, {k} steps, realized "
