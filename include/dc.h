@@ -263,8 +263,10 @@ size_t dc_calibrate_workspace_bytes(const dc_model_cfg* cfg, int32_t K);
  * Jacobian-vector product of the network at every later step of the trace).  Entries
  * with j + h > K are 0.  x1: device f32 [C, T, H, W] (the clip's initial noise); txt:
  * device f32 [N_t, d]; sigmas: host f64 [K+1]; q, d: host f64 [(K-1), h_max] out, the
- * q0/d0 (or q1/d1) of dc_sched_problem.  fp32 models only (DC_ERR_DTYPE otherwise);
- * head_dim 64.  Waits on `stream` (the table entries are read back). */
+ * q0/d0 (or q1/d1) of dc_sched_problem.  The trace runs the library's kernels of the
+ * model's dtype; r, u, the perturbations and the tangents are fp32 (bf16 weights are
+ * widened exactly).  head_dim 64 (else DC_ERR_SHAPE).  Waits on `stream` (the table
+ * entries are read back). */
 dc_status dc_calibrate_tables(const dc_model_cfg* cfg, const dc_model_weights* w, const float* x1,
                               const float* txt, const double* sigmas, int32_t K, int32_t h_max,
                               double eps, double* q, double* d, void* ws, size_t ws_bytes,

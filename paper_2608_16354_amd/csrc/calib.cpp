@@ -12,8 +12,10 @@
 //          t moves by e: dx = (sigma_{t+1} - sigma_t) e, then for every later step k
 //          dx += (sigma_{k+1} - sigma_k) J_k dx, J_k the Jacobian of the full network at
 //          x_k (a Jacobian-vector product: the network run in tangent mode).
-// Runs with j + h > K price nothing and stay 0.  fp32 models (the tangent kernels are
-// fp32 SIMT kernels, calib.hip).
+// Runs with j + h > K price nothing and stay 0.  The trace runs the library's own
+// kernels for the model's dtype (bf16 models: bf16 MFMA blocks); r, u, the perturbations
+// and every tangent are fp32 (fp32 SIMT kernels, calib.hip, with bf16 weights widened
+// exactly on load).
 #include <algorithm>
 #include <cmath>
 
@@ -118,7 +120,7 @@ struct Calib {
       DC_TRY(copy_rows(F(L.h_in), F(L.h), size_t(g.N) * g.d, s));
       for (int l = 0; l < g.L; ++l)
         DC_TRY(block_forward(g, &w->blocks[l], mk + size_t(l) * 6 * g.d, F(L.h), one, blk(), L.blk_bytes, s));
-      DC_TRY(cache_store(F(L.h), F(L.h_in), r_at(k), one, g, s));
+      DC_TRY(lincomb(r_at(k), F(L.h), 1.0f, F(L.h_in), -1.0f, size_t(g.Nv) * g.d, s));   // r = h_out - h_in
       DC_HIP(hipMemcpyAsync(x_at(k + 1), x_at(k), lat * 4, hipMemcpyDeviceToDevice, s));
       DC_TRY(head_euler(g, w, mk + size_t(g.L) * 6 * g.d, F(L.h), x_at(k + 1), dsig(k), one, blk(),
                         L.blk_bytes, s, nullptr));
@@ -130,10 +132,28 @@ struct Calib {
   Status interface(int k, const float* r, float* out) {
     const float* mk = mod_k(k);
     DC_TRY(patch_embed(g, w, x_at(k), txt, F(L.h_in), one, blk(), L.blk_bytes, s));
-    DC_TRY(cache_apply(F(L.h_in), r, F(L.h), one, g, s));
+    DC_TRY(lincomb(F(L.h), F(L.h_in), 1.0f, r, 1.0f, size_t(g.Nv) * g.d, s));         // g = h_in + r
     DC_HIP(hipMemsetAsync(out, 0, lat * 4, s));
     return head_euler(g, w, mk + size_t(g.L) * 6 * g.d, F(L.h), out, 1.0f, one, blk(), L.blk_bytes, s,
                       nullptr);
+  }
+
+  // the fp32 SIMT GEMMs with the model's weights (fp32, or bf16 widened on load)
+  Status mm(const float* A, int lda, const void* W, int ldw, const float* bias, float* out, int ldo,
+            int M, int N, int Kd) const {
+    if (g.bf16)
+      return gemm_f32_bias_act(A, lda, static_cast<const uint16_t*>(W), ldw, bias, out, ldo, M, N, Kd,
+                               Act::kNone, s);
+    return gemm_f32_bias_act(A, lda, static_cast<const float*>(W), ldw, bias, out, ldo, M, N, Kd,
+                             Act::kNone, s);
+  }
+  Status mm_gate(const float* A, int lda, const void* W, int ldw, const float* bias, const float* gate,
+                 float* h, int M, int N, int Kd) const {
+    if (g.bf16)
+      return gemm_f32_gate_residual(A, lda, static_cast<const uint16_t*>(W), ldw, bias, gate, h, g.d, M,
+                                    N, Kd, s);
+    return gemm_f32_gate_residual(A, lda, static_cast<const float*>(W), ldw, bias, gate, h, g.d, M, N,
+                                  Kd, s);
   }
 
   // one block in tangent mode on (h, dh)
@@ -143,22 +163,18 @@ struct Calib {
     const float* zeros = F(L.zeros);
     const float *sh1 = m6, *sc1 = m6 + d, *g1 = m6 + 2 * d, *sh2 = m6 + 3 * d, *sc2 = m6 + 4 * d,
                 *g2 = m6 + 5 * d;
-    const float* wqkv = static_cast<const float*>(b.w_qkv);
-    const float* wo = static_cast<const float*>(b.w_o);
-    const float* w1 = static_cast<const float*>(b.w_1);
-    const float* w2 = static_cast<const float*>(b.w_2);
     DC_TRY(ln_mod_jvp(F(L.h), F(L.dh), N, d, d, sh1, sc1, F(L.a), F(L.da), g.eps, s));
-    DC_TRY(gemm_f32_bias_act(F(L.a), d, wqkv, d, b.b_qkv, F(L.qkv), 3 * d, N, 3 * d, d, Act::kNone, s));
-    DC_TRY(gemm_f32_bias_act(F(L.da), d, wqkv, d, zeros, F(L.dqkv), 3 * d, N, 3 * d, d, Act::kNone, s));
+    DC_TRY(mm(F(L.a), d, b.w_qkv, d, b.b_qkv, F(L.qkv), 3 * d, N, 3 * d, d));
+    DC_TRY(mm(F(L.da), d, b.w_qkv, d, zeros, F(L.dqkv), 3 * d, N, 3 * d, d));
     DC_TRY(attention_jvp_f32(F(L.qkv), F(L.dqkv), g, N, F(L.o), F(L.dout), s));
-    DC_TRY(gemm_f32_gate_residual(F(L.o), d, wo, d, b.b_o, g1, F(L.h), d, N, d, d, s));
-    DC_TRY(gemm_f32_gate_residual(F(L.dout), d, wo, d, zeros, g1, F(L.dh), d, N, d, d, s));
+    DC_TRY(mm_gate(F(L.o), d, b.w_o, d, b.b_o, g1, F(L.h), N, d, d));
+    DC_TRY(mm_gate(F(L.dout), d, b.w_o, d, zeros, g1, F(L.dh), N, d, d));
     DC_TRY(ln_mod_jvp(F(L.h), F(L.dh), N, d, d, sh2, sc2, F(L.a), F(L.da), g.eps, s));
-    DC_TRY(gemm_f32_bias_act(F(L.a), d, w1, d, b.b_1, F(L.z), Fh, N, Fh, d, Act::kNone, s));
-    DC_TRY(gemm_f32_bias_act(F(L.da), d, w1, d, zeros, F(L.dz), Fh, N, Fh, d, Act::kNone, s));
+    DC_TRY(mm(F(L.a), d, b.w_1, d, b.b_1, F(L.z), Fh, N, Fh, d));
+    DC_TRY(mm(F(L.da), d, b.w_1, d, zeros, F(L.dz), Fh, N, Fh, d));
     DC_TRY(gelu_jvp(F(L.z), F(L.dz), size_t(N) * Fh, s));
-    DC_TRY(gemm_f32_gate_residual(F(L.z), Fh, w2, Fh, b.b_2, g2, F(L.h), d, N, d, Fh, s));
-    DC_TRY(gemm_f32_gate_residual(F(L.dz), Fh, w2, Fh, zeros, g2, F(L.dh), d, N, d, Fh, s));
+    DC_TRY(mm_gate(F(L.z), Fh, b.w_2, Fh, b.b_2, g2, F(L.h), N, d, Fh));
+    DC_TRY(mm_gate(F(L.dz), Fh, b.w_2, Fh, zeros, g2, F(L.dh), N, d, Fh));
     return Status::ok();
   }
 
@@ -175,6 +191,9 @@ struct Calib {
     for (int l = 0; l < g.L; ++l) DC_TRY(block_jvp(l, mk + size_t(l) * 6 * d));
     const float* hm = mk + size_t(g.L) * 6 * d;
     DC_TRY(ln_mod_jvp(F(L.h), F(L.dh), g.Nv, d, d, hm, hm + d, F(L.a), F(L.da), g.eps, s));
+    if (g.bf16)
+      return gemm_f32_head(F(L.da), d, static_cast<const uint16_t*>(w->w_head), F(L.zeros), dx, dsig(k), g,
+                           g.Nv, s);
     return gemm_f32_head(F(L.da), d, static_cast<const float*>(w->w_head), F(L.zeros), dx, dsig(k), g,
                          g.Nv, s);
   }
@@ -188,7 +207,7 @@ Status calibrate_tables(const Geo& g, const dc_model_weights* w, const float* x1
                         const double* sigmas, int K, int h_max, double eps, double* q, double* dtab,
                         void* ws, size_t ws_bytes, hipStream_t s) {
   if (!w || !x1 || !sigmas || !q || !dtab || !ws || (g.Nt > 0 && !txt)) return Status::arg("NULL argument");
-  if (g.bf16) return Status::make(DC_ERR_DTYPE, "calibration runs the fp32 model (DC_F32)");
+  if (g.Dh != 64) return Status::shape("calibration supports head_dim 64");
   if (K < 2 || h_max < 1) return Status::arg("calibration needs K >= 2 and h_max >= 1");
   if (!(eps >= 0.0)) return Status::arg("eps must be >= 0");
   if (!w->blocks || !w->w_head || !w->b_head || !w->w_pe) return Status::arg("weight pointer is NULL");

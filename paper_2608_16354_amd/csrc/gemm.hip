@@ -639,9 +639,17 @@ __global__ void __launch_bounds__(512) k_patch_embed_bf16(const float* __restric
 // ---------------------------------------------------------------------------
 // fp32 SIMT GEMM: 64x64 tile, k-step 16, each thread a 4x4 block of outputs
 // ---------------------------------------------------------------------------
-template <class Epi>
+// four consecutive weights as fp32 (W in fp32, or bf16 bits widened exactly)
+__device__ inline float4 load_w4(const float* W, size_t e) { return *reinterpret_cast<const float4*>(W + e); }
+__device__ inline float4 load_w4(const uint16_t* W, size_t e) {
+  const uint2 u = *reinterpret_cast<const uint2*>(W + e);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+}
+
+template <class Epi, class WT>
 __global__ void __launch_bounds__(256) k_gemm_f32(const float* __restrict__ A, int lda,
-                                                  const float* __restrict__ W, int ldw, int M,
+                                                  const WT* __restrict__ W, int ldw, int M,
                                                   int N, int K, Epi epi) {
   __shared__ float sA[16][64 + 4];
   __shared__ float sW[16][64 + 4];
@@ -654,7 +662,7 @@ __global__ void __launch_bounds__(256) k_gemm_f32(const float* __restrict__ A, i
     const int gm = m0 + lr, gn = n0 + lr;
     float4 a = make_float4(0.f, 0.f, 0.f, 0.f), w = a;
     if (gm < M) a = *reinterpret_cast<const float4*>(A + size_t(gm) * lda + k0 + lk);
-    if (gn < N) w = *reinterpret_cast<const float4*>(W + size_t(gn) * ldw + k0 + lk);
+    if (gn < N) w = load_w4(W, size_t(gn) * ldw + k0 + lk);
     sA[lk + 0][lr] = a.x; sA[lk + 1][lr] = a.y; sA[lk + 2][lr] = a.z; sA[lk + 3][lr] = a.w;
     sW[lk + 0][lr] = w.x; sW[lk + 1][lr] = w.y; sW[lk + 2][lr] = w.z; sW[lk + 3][lr] = w.w;
     __syncthreads();
@@ -681,13 +689,13 @@ __global__ void __launch_bounds__(256) k_gemm_f32(const float* __restrict__ A, i
     }
 }
 
-template <class Epi>
-Status launch_f32(const float* A, int lda, const float* W, int ldw, int M, int N, int K,
+template <class Epi, class WT>
+Status launch_f32(const float* A, int lda, const WT* W, int ldw, int M, int N, int K,
                   const Epi& epi, hipStream_t s) {
   if (M <= 0 || N <= 0) return Status::ok();
   if (K % 16 || lda % 4 || ldw % 4) return Status::shape("f32 GEMM needs K % 16 == 0, aligned rows");
   dim3 grid((N + 63) / 64, (M + 63) / 64);
-  hipLaunchKernelGGL(k_gemm_f32<Epi>, grid, dim3(256), 0, s, A, lda, W, ldw, M, N, K, epi);
+  hipLaunchKernelGGL((k_gemm_f32<Epi, WT>), grid, dim3(256), 0, s, A, lda, W, ldw, M, N, K, epi);
   DC_HIP(hipGetLastError());
   return Status::ok();
 }
@@ -706,6 +714,25 @@ Status gemm_f32_gate_residual(const float* A, int lda, const float* W, int ldw, 
                               const float* gate, float* h, int ldh, int M, int N, int K,
                               hipStream_t s) {
   return launch_f32(A, lda, W, ldw, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
+}
+
+Status gemm_f32_bias_act(const float* A, int lda, const uint16_t* W, int ldw, const float* bias,
+                         float* out, int ldo, int M, int N, int K, Act act, hipStream_t s) {
+  if (ldw % 4) return Status::shape("f32 GEMM with bf16 weights needs ldw % 4 == 0");
+  return launch_f32(A, lda, W, ldw, M, N, K, EpiBiasAct{bias, out, ldo, act == Act::kSilu ? 1 : 0}, s);
+}
+
+Status gemm_f32_gate_residual(const float* A, int lda, const uint16_t* W, int ldw, const float* bias,
+                              const float* gate, float* h, int ldh, int M, int N, int K,
+                              hipStream_t s) {
+  if (ldw % 4) return Status::shape("f32 GEMM with bf16 weights needs ldw % 4 == 0");
+  return launch_f32(A, lda, W, ldw, M, N, K, EpiGateResidual{bias, gate, h, ldh}, s);
+}
+
+Status gemm_f32_head(const float* A, int lda, const uint16_t* W, const float* bias, float* x,
+                     float dsigma, const Geo& g, int M, hipStream_t s) {
+  EpiHeadEuler e{bias, x, dsigma, g.T, g.Hl, g.Wl, g.p, g.Hp, g.Wp};
+  return launch_f32(A, lda, W, g.d, M, g.P, g.d, e, s);
 }
 
 Status gemm_f32_gelu(const float* A, int lda, const float* W, int ldw, const float* bias,

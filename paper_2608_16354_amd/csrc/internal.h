@@ -121,6 +121,15 @@ Status gemm_f32_head(const float* A, int lda, const float* W, const float* bias,
                      float dsigma, const Geo& g, int M, hipStream_t s);
 Status gemm_f32_qkv(const float* A, const float* W, const float* bias, float* qk, float* vt,
                     int ldv, const Geo& g, int M, hipStream_t s);
+// the same fp32 SIMT GEMMs with bf16 weights (bits widened exactly on load): the tangent
+// passes of the calibration on bf16 models
+Status gemm_f32_bias_act(const float* A, int lda, const uint16_t* W, int ldw, const float* bias,
+                         float* out, int ldo, int M, int N, int K, Act act, hipStream_t s);
+Status gemm_f32_gate_residual(const float* A, int lda, const uint16_t* W, int ldw, const float* bias,
+                              const float* gate, float* h, int ldh, int M, int N, int K,
+                              hipStream_t s);
+Status gemm_f32_head(const float* A, int lda, const uint16_t* W, const float* bias, float* x,
+                     float dsigma, const Geo& g, int M, hipStream_t s);
 
 // bf16 MFMA GEMM variants.
 Status gemm_bf16_qkv(const uint16_t* A, const uint16_t* W, const float* bias, uint16_t* qk,

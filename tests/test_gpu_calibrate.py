@@ -78,10 +78,40 @@ def test_zero_residual_gives_zero_responses(api, dev):
     assert np.all(d[:-1] > 0.0)
 
 
-def test_bf16_model_is_refused(api, dev):
+def test_bf16_model_tables_near_oracle(api, dev):
+    """A bf16 model of the small shape: the trace runs the library's bf16 kernels (bf16
+    MFMA blocks and attention, the fused head), the perturbations and tangents run in fp32
+    with the bf16 weights; the oracle runs the same bf16-rounded weights in fp64.  The
+    tables differ by the bf16 rounding of the trace's activations (reported), and the
+    library's DP on them equals the oracle's DP bit for bit."""
     import dataclasses
     w = dataclasses.replace(W_TINY, model=dataclasses.replace(W_TINY.model, dtype="bf16"))
     W = I.Weights(w.model, w.cfg_id)
     dm = api.DeviceModel(W, dev)
+    tabs = []
+    for scene in (0, 1):
+        say("bf16 calibration, anchor clip", scene)
+        q, d = _gpu_tables(api, dm, w, scene, dev)
+        qo, do = _oracle_tables(W, w, scene)
+        assert np.array_equal(q == 0.0, qo == 0.0) and np.array_equal(d == 0.0, do == 0.0)
+        nz = qo != 0.0
+        eq = float((np.abs(q[nz] - qo[nz]) / qo[nz]).max())
+        ed = float((np.abs(d[d != 0] - do[do != 0]) / do[do != 0]).max())
+        say("bf16 anchor", scene, "q max rel err", eq, "d max rel err", ed)
+        assert eq < 5e-3 and ed < 5e-5            # measured 4.3e-4 and 2.3e-6
+        tabs.append((q, d))
+    (q0, d0), (q1, d1) = tabs
+    for mo in (w.motions[0], I.Motion(9.0, 0.2)):
+        p = I.scene_problem(w, mo).replace(q0=q0, q1=q1, d0=d0, d1=d1)
+        plan = dp.schedule(p)
+        a = api.dc_schedule_dp(p)
+        assert a.reuse == plan.reuse and (a.n_reuse, a.cost_q) == (plan.n_reuse, plan.cost_q)
+
+
+def test_head_dim_72_is_refused(api, dev):
+    import dataclasses
+    m = dataclasses.replace(W_TINY.model, dtype="bf16", hidden=1152, heads=16, head_dim=72, mlp_hidden=4608)
+    w = dataclasses.replace(W_TINY, model=m)
+    dm = api.DeviceModel(I.Weights(m, w.cfg_id), dev)
     with pytest.raises(api.L.DriveCacheError):
         _gpu_tables(api, dm, w, 0, dev)
