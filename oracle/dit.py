@@ -238,9 +238,17 @@ def block(P: Params, l, mod6, h, rows=None, chunk=256):
     return out
 
 
-def backbone(P: Params, mods, h_in):
-    """F: the whole block stack on h_in [N, d]; returns h_out."""
+def backbone(P: Params, mods, h_in, memo=None):
+    """F: the whole block stack on h_in [N, d]; returns h_out.
+    memo (optional, for long runs that may be interrupted): an object whose
+    load(l, h) returns block l's output for the input h if it holds it (else None)
+    and whose save(l, h, out) records it; the values are those of block() itself."""
     h = h_in
     for l in range(P.m.n_blocks):
-        h = block(P, l, mods[l], h)
+        out = memo.load(l, h) if memo is not None else None
+        if out is None:
+            out = block(P, l, mods[l], h)
+            if memo is not None:
+                memo.save(l, h, out)
+        h = out
     return h

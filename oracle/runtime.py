@@ -80,7 +80,7 @@ def drift_value(sums, eps, metric="l1"):
 
 def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
            W_low=None, k_switch=None, guidance=None, txt_null=None, steps=None, on_step=None,
-           resume=None):
+           resume=None, block_memo=None):
     """One cached K-step sample of one scene.
 
     W: `Weights`; x1 [C,T,H,W]; txt [n_txt, d]; sigmas [K+1]; prob: `SchedProblem`.
@@ -95,7 +95,8 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
     the records so far, the current plan and the whole controller state (a dict), for
     writing intermediate results.
     resume: such a state dict; the sample continues after its step (a long run can be
-    stopped and picked up again without recomputing the executed steps)."""
+    stopped and picked up again without recomputing the executed steps).
+    block_memo: passed to dit.backbone for the conditional branch (see there)."""
     experts = [dit.Params(W)]
     if W_low is not None:
         if prob.segment is None or prob.segment[k_switch - 1] == prob.segment[k_switch - 2]:
@@ -151,7 +152,7 @@ def sample(W, x1, txt, sigmas, prob, metric="l1", uncached=False, force_veto=(),
             g = h_in[: m.n_v] + r
             g_u = h_in_u[: m.n_v] + r_u if cfg else None
         else:
-            h_out = dit.backbone(P, mods, h_in)
+            h_out = dit.backbone(P, mods, h_in, memo=block_memo)
             r = h_out[: m.n_v] - h_in[: m.n_v]
             g = h_out[: m.n_v]
             if cfg:

@@ -13,9 +13,12 @@ charge, the budget tau and a fingerprint of the generated inputs.  With
 --every-step the file is rewritten after each step (a long run leaves a valid
 truncated artefact at every point); with --checkpoint the whole controller state is
 saved after each step to that file (this script's own pickle) and a run started
-with an existing checkpoint continues after its step.
+with an existing checkpoint continues after its step; --block-dir additionally keeps
+each block's output of the step in progress (keyed by the sha256 of the block's
+input), so an interrupted refresh step picks up after its last finished block.
 """
 import argparse
+import hashlib
 import os
 import pickle
 import sys
@@ -63,6 +66,32 @@ def _write(path, name, thr, tau, fp, k, x, records, plan, seconds):
     os.replace(tmp, path)
 
 
+class BlockStore:
+    """Block outputs of the refresh step in progress, on disk, keyed by the block index
+    and the sha256 of the block's input (a stale entry never matches)."""
+
+    def __init__(self, root):
+        self.root = root
+        os.makedirs(root, exist_ok=True)
+
+    def _key(self, l, h):
+        return os.path.join(self.root, f"block{l:03d}-{hashlib.sha256(h.tobytes()).hexdigest()[:32]}.npy")
+
+    def load(self, l, h):
+        path = self._key(l, h)
+        return np.load(path, allow_pickle=False) if os.path.exists(path) else None
+
+    def save(self, l, h, out):
+        path = self._key(l, h)
+        np.save(path + ".tmp.npy", out)
+        os.replace(path + ".tmp.npy", path)
+
+    def clear(self):
+        for f in os.listdir(self.root):
+            if f.startswith("block"):
+                os.remove(os.path.join(self.root, f))
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("name", nargs="?", default="dit-12x1152-bf16")
@@ -71,6 +100,7 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=None, help="stop after this many steps")
     ap.add_argument("--every-step", action="store_true", help="rewrite the file after every step")
     ap.add_argument("--checkpoint", default=None, help="state file to save after each step and resume from")
+    ap.add_argument("--block-dir", default=None, help="directory for the block outputs of the step in progress")
     a = ap.parse_args(argv)
     w = I.WORKLOADS[a.name]
     thr = w.thr if a.thr is None else a.thr
@@ -88,6 +118,8 @@ def main(argv=None):
             resume = pickle.load(f)
         print(f"{a.name}: resuming after step {resume['k']}", flush=True)
 
+    store = BlockStore(a.block_dir) if a.block_dir else None
+
     def on_step(k, x, records, plan, state):
         W.drop()          # the oracle keeps its own float64 copies of every tensor it used
         if a.checkpoint:
@@ -95,6 +127,8 @@ def main(argv=None):
             with open(tmp, "wb") as f:
                 pickle.dump(state, f, protocol=pickle.HIGHEST_PROTOCOL)
             os.replace(tmp, a.checkpoint)
+        if store is not None:
+            store.clear()                 # the step is in the checkpoint
         r = records[-1]
         d = "" if r.drift is None else f" drift {r.drift:.6f} thr {r.threshold:.4f}"
         print(f"{a.name} step {k}: {'reuse' if r.realized else 'full'}{' (vetoed)' if r.vetoed else ''}"
@@ -103,7 +137,8 @@ def main(argv=None):
             _write(path, a.name, thr, tau, fp, k, x, records, plan, time.time() - t0)
 
     res = runtime.sample(W, I.latent(w.model, w.cfg_id, 0), I.text(w.model, w.cfg_id, 0),
-                         I.sigmas(w.K), p, steps=a.steps, on_step=on_step, resume=resume)
+                         I.sigmas(w.K), p, steps=a.steps, on_step=on_step, resume=resume,
+                         block_memo=store)
     k = len(res.records)
     _write(path, a.name, thr, tau, fp, k, res.x, res.records, res.plan, time.time() - t0)
     print(f"{a.name}: {time.time() - t0:.1f} s, {k} steps, realized "
