@@ -96,3 +96,28 @@ def test_sampler_options_are_validated_before_any_device_work():
     # an unknown option value
     o = _lib.SamplerOpts(); o.cfg = 2
     assert create([p], o)[0] == _lib.DC_ERR_ARG
+
+
+def test_calibration_and_noalloc_entry_points_validate_on_the_host():
+    """dc_calibrate_tables and dc_drift_l1_noalloc refuse bad arguments before any device
+    work (no GPU here: every case below must fail on the host)."""
+    import ctypes as C
+    lib = _lib.load()
+    cfg = _lib.ModelCfg(2, 256, 4, 64, 1024, 16, 4, 16, 16, 2, 16, 0, 1e-6)
+    assert lib.dc_calibrate_workspace_bytes(C.byref(cfg), 10) > 0
+    assert lib.dc_calibrate_workspace_bytes(C.byref(cfg), 0) == 0
+    q = (C.c_double * 18)()
+    d = (C.c_double * 18)()
+    sig = (C.c_double * 11)()
+    rc = lib.dc_calibrate_tables(C.byref(cfg), None, None, None, sig, 10, 2, 1e-6, q, d, None, 0, None)
+    assert rc == _lib.DC_ERR_ARG and b"NULL" in lib.dc_last_error()
+    h72 = _lib.ModelCfg(2, 1152, 16, 72, 4608, 16, 4, 16, 16, 2, 16, 1, 1e-6)
+    w = _lib.ModelWeights()
+    fake = C.c_void_p(0x1000)
+    rc = lib.dc_calibrate_tables(C.byref(h72), C.byref(w), fake, fake, sig, 10, 2, 1e-6, q, d, fake, 0, None)
+    assert rc == _lib.DC_ERR_SHAPE
+    idx = (C.c_int32 * 65)(*range(65))
+    rc = lib.dc_drift_l1_noalloc(C.byref(cfg), fake, fake, fake, 0, fake, idx, 65, None)
+    assert rc == _lib.DC_ERR_ARG
+    rc = lib.dc_drift_l1_noalloc(C.byref(cfg), None, fake, fake, 0, fake, idx, 1, None)
+    assert rc == _lib.DC_ERR_ARG
