@@ -282,7 +282,9 @@ typedef struct {
   float* x;          /* [B, C, T, H, W] latent x_k, updated in place */
   const float* txt;  /* [B, N_t, d] text embeddings */
   float* h_in;       /* [B, N, d] backbone input */
-  float* h;          /* [B, N, d] residual stream (also the head input) */
+  float* h;          /* [B, N, d] residual stream; the head input on refresh steps (on reuse
+                        steps bf16 models with hidden <= 2048 form g = h_in + r inside the
+                        head kernel and leave h as it was; other models write g here) */
   void* resid;       /* [B, N_v, d] residual cache r_j (model dtype) */
   void* u_ref;       /* [B, N_v, d] refresh input u_j (model dtype) */
   float* mod;        /* [K, L+1, 6, d] modulation table (filled at creation) */
