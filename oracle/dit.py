@@ -173,12 +173,16 @@ def euler(x, v, s0, s1):
 # attention and the transformer block
 # ----------------------------------------------------------------------------
 def attention_rows(q, k, v):
-    """softmax(q k^T / sqrt(d_h)) v for one head; q [r, d_h], k, v [N, d_h]."""
-    s = (q @ k.T) / math.sqrt(q.shape[1])
-    s = s - s.max(axis=1, keepdims=True)
-    p = np.exp(s)
-    p = p / p.sum(axis=1, keepdims=True)
-    return p @ v
+    """softmax(q k^T / sqrt(d_h)) v for one head; q [r, d_h], k, v [N, d_h].
+    The steps run in place in the one score array (the same operations in the same
+    order as with fresh arrays, so the same values; large fresh arrays cost page
+    faults that serialise the worker threads)."""
+    s = q @ k.T
+    s /= math.sqrt(q.shape[1])
+    s -= s.max(axis=1, keepdims=True)
+    np.exp(s, out=s)
+    s /= s.sum(axis=1, keepdims=True)
+    return s @ v
 
 
 def attention(q, k, v, heads, chunk=2048):
