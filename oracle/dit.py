@@ -173,41 +173,54 @@ def euler(x, v, s0, s1):
 # attention and the transformer block
 # ----------------------------------------------------------------------------
 def attention_rows(q, k, v):
-    """softmax(q k^T / sqrt(d_h)) v for one head; q [r, d_h], k, v [N, d_h].
-    The steps run in place in the one score array (the same operations in the same
-    order as with fresh arrays, so the same values; large fresh arrays cost page
-    faults that serialise the worker threads)."""
-    s = q @ k.T
-    s /= math.sqrt(q.shape[1])
+    """softmax(q k^T / sqrt(d_h)) v for one head; q [r, d_h], k, v [N, d_h]."""
+    return _softmax_times_v(q @ k.T, v, q.shape[1])
+
+
+def _softmax_times_v(s, v, dh):
+    """softmax(s / sqrt(d_h)) v for scores s = q k^T.  The steps run in place in s
+    (the same operations in the same order as with fresh arrays, so the same values;
+    large fresh arrays cost page faults that serialise the worker threads)."""
+    s /= math.sqrt(dh)
     s -= s.max(axis=1, keepdims=True)
     np.exp(s, out=s)
     s /= s.sum(axis=1, keepdims=True)
     return s @ v
 
 
-def attention(q, k, v, heads, chunk=2048):
+def split_heads(k, v, heads):
+    """Per head: (k_h^T, v_h) as contiguous arrays [d_h, N] and [N, d_h].  The same
+    values as the column slices of k and v; the products read them faster."""
+    dh = k.shape[1] // heads
+    return [(np.ascontiguousarray(k[:, h * dh:(h + 1) * dh].T), np.ascontiguousarray(v[:, h * dh:(h + 1) * dh]))
+            for h in range(heads)]
+
+
+def attention(q, k, v, heads, chunk=2048, kv_heads=None):
     """Multi-head attention over all rows; q [r, d], k, v [N, d] (heads concatenated).
-    Query rows are processed in chunks only to bound memory (rows are independent)."""
+    Query rows are processed in chunks only to bound memory (rows are independent).
+    kv_heads (optional): split_heads(k, v, heads), which replaces k and v."""
     r, d = q.shape
     dh = d // heads
     out = np.empty((r, d), F)
     for hd in range(heads):
         sl = slice(hd * dh, (hd + 1) * dh)
-        kh, vh = k[:, sl], v[:, sl]
+        kt, vh = (k[:, sl].T, v[:, sl]) if kv_heads is None else kv_heads[hd]
         for a in range(0, r, chunk):
-            out[a: a + chunk, sl] = attention_rows(q[a: a + chunk, sl], kh, vh)
+            out[a: a + chunk, sl] = _softmax_times_v(q[a: a + chunk, sl] @ kt, vh, dh)
     return out
 
 
-def _block_rows(P: Params, l, mod6, h, a, k, v):
+def _block_rows(P: Params, l, mod6, h, a, kv_heads):
     """The part of block l after the keys and values: rows h, with modulated input a,
-    attend to every row's k, v; each output row depends on its own row only."""
+    attend to every row's keys and values (kv_heads = split_heads(k, v)); each output
+    row depends on its own row only."""
     d = P.m.hidden
     eps = P.m.ln_eps
     _, _, gate1, shift2, scale2, gate2 = mod6
     wq, bq = P.b(l, "w_qkv"), P.b(l, "b_qkv")
     q = a @ wq[:d].T + bq[:d]
-    o = attention(q, k, v, P.m.heads)
+    o = attention(q, None, None, P.m.heads, chunk=64, kv_heads=kv_heads)
     hr = h + gate1 * (o @ P.b(l, "w_o").T + P.b(l, "b_o"))
     a2 = modulate(hr, shift2, scale2, eps)
     z = gelu_tanh(a2 @ P.b(l, "w_1").T + P.b(l, "b_1"))
@@ -225,15 +238,15 @@ def block(P: Params, l, mod6, h, rows=None, chunk=256):
     a = _by_rows(modulate, h, shift1, scale1, P.m.ln_eps)
     wq, bq = P.b(l, "w_qkv"), P.b(l, "b_qkv")
     kv = a @ wq[d:].T + bq[d:]                 # keys and values of every row
-    k = np.ascontiguousarray(kv[:, :d])
-    v = np.ascontiguousarray(kv[:, d:])
+    kv_heads = split_heads(kv[:, :d], kv[:, d:], P.m.heads)
+    del kv
     sel = np.arange(h.shape[0]) if rows is None else np.arange(h.shape[0])[rows]
     out = np.empty((len(sel), d), F)
     starts = range(0, len(sel), chunk)
 
     def run(s):
         rr = sel[s: s + chunk]
-        out[s: s + chunk] = _block_rows(P, l, mod6, h[rr], a[rr], k, v)
+        out[s: s + chunk] = _block_rows(P, l, mod6, h[rr], a[rr], kv_heads)
 
     for name in ("w_o", "b_o", "w_1", "b_1", "w_2", "b_2"):
         P.b(l, name)                           # load once, before the threads share P
