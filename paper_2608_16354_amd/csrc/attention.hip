@@ -689,15 +689,6 @@ k_attn16(const uint16_t* __restrict__ qk, const uint16_t* __restrict__ vt, int l
   }
 }
 
-// Zero the padding columns [M, ldv) of the transposed values (never written by
-// the QKV GEMM; the attention DMA reads them and multiplies them by zero).
-__global__ void k_zero_vt_tail(uint16_t* vt, int rows, int ldv, int M) {
-  const int w = ldv - M;
-  const size_t n = size_t(rows) * w;
-  for (size_t e = size_t(blockIdx.x) * blockDim.x + threadIdx.x; e < n; e += size_t(gridDim.x) * blockDim.x)
-    vt[(e / w) * ldv + M + (e % w)] = 0;
-}
-
 // fp32 path: one thread per query row, key/value tiles of 64 tokens in LDS.
 template <int D>
 __global__ void __launch_bounds__(64) k_attn_f32(const float* __restrict__ qk,
@@ -807,11 +798,7 @@ static Status launch_attn(const uint16_t* qk, const uint16_t* vt, int ldv, uint1
 Status attention_bf16(const uint16_t* qk, const uint16_t* vt, int ldv, uint16_t* out,
                       const Geo& g, int M, float* part, size_t part_bytes, hipStream_t s) {
   if (ldv % 64 || ldv < M) return Status::shape("attention needs ldv >= M, ldv % 64 == 0");
-  if (ldv > M) {
-    uint16_t* v = const_cast<uint16_t*>(vt);
-    hipLaunchKernelGGL(k_zero_vt_tail, dim3(64), dim3(256), 0, s, v, g.d, ldv, M);
-    DC_HIP(hipGetLastError());
-  }
+  // the padding tokens [M, ldv) of vt hold zeros: the bf16 QKV GEMM writes them
   // head_dim 64: the 16x16x32 kernel from 8,192 tokens (MI355X, 17,776 x 30 heads: 1.96 vs
   // 2.08 ms); below that its per-item first-tile pass costs more than it saves (3,597 x 30:
   // 121 vs 119 us)

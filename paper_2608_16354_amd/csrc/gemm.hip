@@ -111,7 +111,10 @@ struct EpiQKVBf16 {
           if (mb + 8 * (i >> 2) + (i & 3) < M) q[size_t(8 * (i >> 2) + (i & 3)) * 2 * d] = to_bf16((v[i] + b) * sc);
       }
     } else {
-      // V^T row n - 2d: four consecutive tokens per 8-byte store (ldv and mb are multiples of 4)
+      // V^T row n - 2d: four consecutive tokens per 8-byte store (ldv and mb are multiples of 4).
+      // The padding tokens [M, ldv) get zeros: the attention's last value tile reads them
+      // (and multiplies them by zero probabilities, which NaN garbage would turn into NaN).
+      // The last row tile always reaches ldv (tile heights are multiples of 64).
       uint16_t* __restrict__ r = vt + size_t(n - 2 * d) * ldv + mb;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -122,8 +125,11 @@ struct EpiQKVBf16 {
           *reinterpret_cast<uint2*>(r + 8 * g) = pk;
         } else {
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (mb + 8 * g + j < M) r[8 * g + j] = to_bf16(v[4 * g + j] + b);
+          for (int j = 0; j < 4; ++j) {
+            const int m = mb + 8 * g + j;
+            if (m < M) r[8 * g + j] = to_bf16(v[4 * g + j] + b);
+            else if (m < ldv) r[8 * g + j] = 0;
+          }
         }
       }
     }
