@@ -186,12 +186,14 @@ def _stored_oracle(name, tag=None):
     return w, gold
 
 
-def _check_sample_against_stored_oracle(api, dev, name, tag=None, min_steps=1):
+def _check_sample_against_stored_oracle(api, dev, name, tag=None, min_steps=1, batch_with=None):
     """Run the library's sampler for the stored number of steps, on the stored threshold,
     in the launch configuration the benchmark uses (SamplerBuffers + Sampler), and compare:
     realized masks, vetoes and the plan bit-exactly; every drift against the oracle's with
     the error below the oracle's margin to its threshold (so no decision can flip); the
-    latent within rel-L2 2e-2."""
+    latent within rel-L2 2e-2.  batch_with (a batch workload): the stored scene runs as
+    scene 0 of a batch whose other scenes are that workload's scenes 1, 2, ... (their own
+    motions and inputs), and scene 0 is compared."""
     w, gold = _stored_oracle(name, tag)
     S = int(gold["steps"]) if "steps" in gold.files else w.K
     if S < min_steps:
@@ -204,16 +206,25 @@ def _check_sample_against_stored_oracle(api, dev, name, tag=None, min_steps=1):
     W = I.Weights(w.model, w.cfg_id)
     say("upload", name)
     dm = api.DeviceModel(W, dev)
-    x1, txt = I.latent(w.model, w.cfg_id, 0), I.text(w.model, w.cfg_id, 0)
-    say("sample", name, tag or "", "steps", S, "thr", thr)
-    x, rs, ds, plans = run_gpu(api, dm, w, [p], x1[None], txt[None], steps=S)
+    probs, seeds, wr = [p], [0], w
+    if batch_with is not None:
+        wb = I.WORKLOADS[batch_with]
+        assert wb.model == w.model and wb.K == w.K
+        probs += [I.scene_problem(wb, m, tau_q=tau) for m in I.scene_motions(wb)[1:]]
+        seeds += list(range(1, wb.batch))
+        wr = wb
+    x1 = np.stack([I.latent(w.model, w.cfg_id, s) for s in seeds])
+    txt = np.stack([I.text(w.model, w.cfg_id, s) for s in seeds])
+    say("sample", name, tag or "", "scenes", len(probs), "steps", S, "thr", thr)
+    x, rs, ds, plans = run_gpu(api, dm, wr, probs, x1, txt, steps=S)
     del dm
     assert rs[:, 0].tolist() == gold["realized"][:S].tolist()          # bit-exact mask
     d = gold["drift"][:S]
     chk = ~np.isnan(d)
     assert np.array_equal(np.isnan(ds[:, 0]), ~chk)
     err = np.abs(ds[chk, 0] - d[chk])
-    report = {"steps": S, "checks": int(chk.sum()), "max_drift_err": float(err.max()) if chk.any() else 0.0}
+    report = {"steps": S, "checks": int(chk.sum()), "max_drift_err": float(err.max()) if chk.any() else 0.0,
+              "masks": ["".join(map(str, rs[:, b])) for b in range(len(probs))]}
     if "threshold" in gold.files:
         margin = np.abs(d[chk] - gold["threshold"][:S][chk])
         report["min_margin"] = float(margin.min()) if chk.any() else None
@@ -249,6 +260,16 @@ def test_target_sample_matches_stored_oracle(api, dev):
     attention kernel) for the steps the stored oracle sample covers: bit-exact realized
     mask, plan and vetoes, every drift inside the oracle's margin, latent rel-L2 <= 2e-2."""
     _check_sample_against_stored_oracle(api, dev, "dit-30x1920-bf16", min_steps=8)
+
+
+def test_target_scene_in_a_batch_matches_stored_oracle(api, dev):
+    """The same stored 30-block sample as scene 0 of a 4-scene batch (the other scenes
+    with their own motions, inputs and masks): masked batch dispatch at full size keeps
+    scene 0 on the oracle's mask, drifts and latent."""
+    rep = _check_sample_against_stored_oracle(api, dev, "dit-30x1920-bf16", min_steps=8,
+                                              batch_with="dit-30x1920-bf16-b4")
+    assert rep["checks"] >= 1
+    assert len(set(rep["masks"])) > 1                 # the scenes' masks differ: dispatch is masked
 
 
 def test_mid_bf16_legality_variants_reduce_to_the_plain_sampler(api, dev):
