@@ -187,8 +187,8 @@ def main():
                     help="first run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(see DESIGN.md for how the step would shard)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path, "
+              "so no figure for more than one GPU is measured", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -41,7 +41,7 @@ def test_run_record_thresholds_follow_the_runs():
 
 def test_algorithmic_counts_at_the_bench_shape():
     m = I.WORKLOADS["dit-30x1920-bf16"].model
-    # 4 N^2 d for attention, 24 N d^2 for the four GEMMs at MLP 4d (SURVEY shape: 17,776 x 1920)
+    # 4 N^2 d for attention, 24 N d^2 for the four GEMMs at MLP 4d (the bench shape: 17,776 x 1920)
     assert bench.attention_flops(m) == 4.0 * 17776 ** 2 * 1920
     assert bench.gemm_flops(m) == 24.0 * 17776 * 1920 ** 2
     hb = bench.hbm_bytes(m)
