@@ -106,10 +106,10 @@ def host_info():
     return model, blas
 
 
-def cpu_baseline(w, W, schedule, budget_s=30.0):
+def cpu_baseline(w, W, schedule, budget_s=10.0):
     """The fp64 oracle on a bounded sample of the same workload, extrapolated to one
-    cached sample: one block at full length on two query-row subsets (2048 and 8192 rows) (the per-block
-    cost is fixed key/value work plus a per-row cost) and one full reuse step."""
+    cached sample: whole blocks at full length (all rows; blocks 0, 1, 2 until budget_s
+    of block time is spent) and one full reuse step."""
     import numpy as np
     from oracle import dit
     from paper_2608_16354_amd import inputs as I
@@ -118,16 +118,16 @@ def cpu_baseline(w, W, schedule, budget_s=30.0):
     P = dit.Params(W)
     mods, head_mod = dit.step_modulation(P, 0.5)
     h = I.hidden_state(m, (90,)).astype(np.float64)
-    rng = np.random.default_rng(0)
-    times = {}
-    for R in (2048, 8192):
-        rows = np.sort(rng.choice(m.n_tok, R, replace=False))
+    times = []
+    for l in range(min(3, m.n_blocks)):
+        for name in ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2"):
+            P.b(l, name)                                 # weights made before the clock starts
         t0 = time.perf_counter()
-        dit.block(P, 0, mods[0], h, rows=rows)
-        times[R] = time.perf_counter() - t0
-    per_row = (times[8192] - times[2048]) / (8192 - 2048)
-    fixed = max(times[2048] - 2048 * per_row, 0.0)
-    t_block = fixed + m.n_tok * per_row
+        dit.block(P, l, mods[l], h)
+        times.append(time.perf_counter() - t0)
+        if sum(times) >= budget_s:
+            break
+    t_block = sum(times) / len(times)
     x = I.latent(m, w.cfg_id, 0).astype(np.float64)
     txt = I.text(m, w.cfg_id, 0)
     t0 = time.perf_counter()
@@ -141,12 +141,12 @@ def cpu_baseline(w, W, schedule, budget_s=30.0):
     n_reu = len(schedule) - n_ref
     t_sample = n_ref * (m.n_blocks * t_block + t_reuse) + n_reu * t_reuse
     cores = min(16, len(os.sched_getaffinity(0)))     # the oracle's worker and BLAS threads
-    spent = sum(times.values()) + t_reuse
+    spent = sum(times) + t_reuse
     cpu, blas = host_info()
     return {"value": w.batch * m.n_v * w.K / (w.batch * t_sample), "unit": "latent token*steps/s",
             "cores": cores, "kind": "oracle", "dtype": "f64", "cpu_model": cpu, "blas": blas,
-            "sample": (f"fp64 oracle: one block at {m.n_tok} tokens on 2048 and 8192 query rows "
-                       f"({times[2048]:.1f}s, {times[8192]:.1f}s) + one full reuse step ({t_reuse:.1f}s), "
+            "sample": (f"fp64 oracle: {len(times)} whole block(s) at {m.n_tok} tokens "
+                       f"({', '.join(f'{t:.1f}s' for t in times)}) + one full reuse step ({t_reuse:.1f}s), "
                        f"extrapolated to the {n_ref}-refresh/{n_reu}-reuse schedule; {spent:.0f}s of CPU work")}
 
 
